@@ -1,0 +1,200 @@
+"""Pins of the BF16 algorithm model (oracle.algo_model) against the paper.
+
+The model is the step-by-step statement of the paper's forward (eq.
+gproj-forward) and Algorithm 1 backward with the implemented rounding points.
+It is pinned by: an independent brute-force BF16 rounding check, the -24
+witness values the paper prints, the exact-arithmetic limit (equals the exact
+FP64 oracle), Proposition 4.1's algebraic properties, the two-key bound, and
+the synthetic offset sweep floor the paper reports.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synthetic as S
+from oracle import algo_model as M
+
+pytestmark = pytest.mark.filterwarnings("ignore::RuntimeWarning")
+
+
+def _bf16_nearest_bruteforce(x: float) -> float:
+    """Nearest BF16 value by enumeration of neighbours; ties to even mantissa."""
+    f = np.float32(x)
+    bits = int(np.array([f]).view(np.uint32)[0])
+    base = bits & 0xFFFF0000
+    cands = []
+    for cb in (base - 0x10000, base, base + 0x10000):
+        if cb < 0 or cb > 0xFFFFFFFF:
+            continue
+        val = float(np.array([cb], dtype=np.uint32).view(np.float32)[0])
+        if np.isfinite(val):
+            cands.append((abs(val - float(f)), (cb >> 16) & 1, val))
+    cands.sort()
+    best = [c for c in cands if c[0] == cands[0][0]]
+    if len(best) > 1:
+        best = [c for c in best if c[1] == 0]
+    return best[0][2]
+
+
+def test_bf16_round_against_bruteforce():
+    rng = np.random.default_rng(1)
+    xs = np.concatenate([rng.standard_normal(2000) * 10.0 ** rng.integers(-6, 6, 2000),
+                         np.array([1 + 2 ** -8, 1 + 3 * 2 ** -8, 1 + 3 / 1024, -0.125732421875,
+                                   65536.0, 2 ** -126, 3.0e38])])
+    got = M.bf16_round(xs.astype(np.float32))
+    for x, g in zip(xs, got):
+        assert g == _bf16_nearest_bruteforce(x), x
+    # ties to even, and the paper's example: 1 + 3/1024 rounds to 1
+    assert M.bf16_round(np.float32([1 + 2 ** -8]))[0] == 1.0
+    assert M.bf16_round(np.float32([1 + 3 * 2 ** -8]))[0] == np.float32(1 + 2 ** -6)
+    assert M.bf16_round(np.float32([1 + 3 / 1024]))[0] == 1.0
+
+
+def _witness(golden_dir):
+    with open(os.path.join(golden_dir, "witness_minus24.json")) as f:
+        w = json.load(f)
+    pb = w["printed_by_paper"]
+    N, d = 4, 64
+    q = np.zeros((N, d), np.float32); k = np.zeros((N, d), np.float32)
+    v = np.zeros((N, d), np.float32); u = np.zeros((N, d), np.float32)
+    k[:, :2] = pb["k"]; v[:, :2] = pb["v"]; u[3, :2] = pb["u"]
+    return w, q, k, v, u
+
+
+def test_witness_through_the_model(golden_dir):
+    """Plain contracts the cast operand and returns -24; GProj returns exactly 0
+    (Section 3.4, appendix A, Section 5.2 'on the four-key example ... exactly zero')."""
+    w, q, k, v, u = _witness(golden_dir)
+    pb, hand = w["printed_by_paper"], w["derived_by_hand_from_printed_values"]
+    alpha = pb["alpha"]
+    out = {}
+    for mode in M.MODES:
+        O, LSE, dQ, dK, dV, st = M.forward_backward(q, k, v, u, True, alpha, mode)
+        out[mode] = (O, dQ, dK, dV, st)
+    O, dQ, dK, dV, st = out["plain"]
+    assert list(O[3, :2]) == pb["o"]
+    assert list(st["t"][3, :4]) == pb["t_bf16"]
+    assert st["rho"][3] == pb["rho"]
+    assert np.float32(alpha) * st["A"][3, 0] == pb["plain_dq_first_coordinate"]
+    assert list(dQ[3, :2]) == hand["plain_dq_bf16"]
+    for mode in ("gproj_q", "gproj"):
+        _, dQg, dKg, dVg, stg = out[mode]
+        assert dQg[3, 0] == 0.0
+        assert list(dQg[3, :2]) == hand["gproj_dq_bf16"]
+        assert stg["lam"][3] == np.float32(-pb["eta"])
+        assert np.abs(dKg).max() == 0.0
+        assert np.all(dVg[:, :2] == 0.25)
+
+
+def test_model_mode_identities():
+    """gproj_q leaves dK, dV as plain; the key pass leaves dQ, dV as gproj_q
+    (Section 5.2; appendix 'Backward-only comparison')."""
+    w = S.WORKLOADS[1]
+    x = S.make_inputs(w, 1001)
+    q, k, v, u = (S.bf16_bits_to_f32(x[n][0, 0]) for n in ("q", "k", "v", "do"))
+    res = {m: M.forward_backward(q, k, v, u, True, w.scale, m) for m in M.MODES}
+    assert np.array_equal(res["plain"][3], res["gproj_q"][3])
+    assert np.array_equal(res["plain"][4], res["gproj_q"][4])
+    assert np.array_equal(res["gproj_q"][2], res["gproj"][2])
+    assert np.array_equal(res["gproj_q"][4], res["gproj"][4])
+    assert not np.array_equal(res["plain"][2], res["gproj"][2])
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_model_exact_limit_equals_oracle(causal):
+    """With every cast the identity and FP64 arithmetic, the model is the exact VJP."""
+    rng = np.random.default_rng(2)
+    N, d = 70, 16
+    q = rng.standard_normal((N, d)); k = rng.standard_normal((N, d)) + 5 * rng.standard_normal(d)
+    v = rng.standard_normal((N, d)); u = rng.standard_normal((N, d))
+    ex = oracle.exact(q[None], k[None], v[None], u[None], causal, 0.3)
+    for mode in M.MODES:
+        O, LSE, dQ, dK, dV, st = M.forward_backward(q, k, v, u, causal, 0.3, mode, rounding=False)
+        for n, a in zip(("O", "LSE", "dQ", "dK", "dV"), (O, LSE, dQ, dK, dV)):
+            ref = ex[n][0]
+            assert np.linalg.norm(a - ref) <= 1e-11 * max(1.0, np.linalg.norm(ref)), (mode, n)
+
+
+def test_projection_properties():
+    """Proposition 4.1: Pi_r idempotent, 1^T Pi_r = 0, t - lambda r has zero row
+    sum, the query contraction equals alpha sum_j t_j (k_j - mu_r) and is
+    unchanged by a common key translation at fixed t, r; t - lambda r is the
+    minimum of sum (z - t)^2 / r over zero-sum z."""
+    rng = np.random.default_rng(4)
+    L, d, alpha = 50, 8, 0.7
+    r = rng.random(L) + 0.01
+    t = rng.standard_normal(L)
+    K = rng.standard_normal((L, d))
+    m = r.sum()
+    Pi = np.eye(L) - np.outer(r, np.ones(L)) / m
+    assert np.allclose(Pi @ Pi, Pi, atol=1e-13)
+    assert np.allclose(np.ones(L) @ Pi, 0, atol=1e-13)
+    tp = Pi @ t
+    assert abs(tp.sum()) < 1e-12
+    assert np.allclose(tp, t - (t.sum() / m) * r, atol=1e-13)
+    G = M.project_query_row(t, r, K, alpha)
+    mu_r = (r @ K) / m
+    assert np.allclose(G, alpha * (t @ (K - mu_r)), atol=1e-12)
+    b = rng.standard_normal(d) * 1e4
+    assert np.allclose(M.project_query_row(t, r, K + b, alpha), G, rtol=0, atol=1e-8)
+    # minimum r-weighted norm among zero-sum vectors: perturb along zero-sum directions
+    base = np.sum((tp - t) ** 2 / r)
+    for _ in range(20):
+        e = rng.standard_normal(L); e -= e.mean()
+        assert np.sum((tp + 1e-3 * e - t) ** 2 / r) >= base
+
+
+def test_two_key_row_mass_bound():
+    """Eq. two-key: |rho| <= 2 u_b eps(1-eps)|a1 - a2| for the BF16 cast t of g."""
+    rng = np.random.default_rng(6)
+    ub = 2.0 ** -8
+    for _ in range(2000):
+        eps = rng.random() * 0.5
+        a1, a2 = rng.standard_normal(2) * 10.0 ** rng.integers(-3, 3)
+        p = np.array([1 - eps, eps])
+        a = np.array([a1, a2])
+        g = p * (a - p @ a)
+        t = M.bf16_round(g.astype(np.float32)).astype(np.float64)
+        rho = t.sum()
+        assert abs(rho) <= 2 * ub * eps * (1 - eps) * abs(a1 - a2) * (1 + 1e-6)
+
+
+def _offset_sweep(std, offsets, rows, L=1024, d=64, seed=0):
+    """Appendix D 'Synthetic offset sweep': exact FP64 forward and score gradient,
+    t = BF16(g), r = BF16(p); per-row relative dq error, median over rows."""
+    rng = np.random.default_rng(seed)
+    out = {}
+    for nb in offsets:
+        eg, ef = [], []
+        for _ in range(rows):
+            z = rng.standard_normal((L, d))
+            dirb = rng.standard_normal(d); dirb /= np.linalg.norm(dirb)
+            K = z + nb * dirb
+            q = rng.standard_normal(d); q *= std / np.linalg.norm(q)
+            s = K @ q
+            p = np.exp(s - s.max()); p /= p.sum()
+            a = rng.standard_normal((L, d)) @ rng.standard_normal(d)
+            g = p * (a - p @ a)
+            G = g @ K
+            t = M.bf16_round(g.astype(np.float32)).astype(np.float64)
+            r = M.bf16_round(p.astype(np.float32)).astype(np.float64)
+            Gf = t @ K
+            Gp = M.project_query_row(t, r, K, 1.0)
+            eg.append(np.linalg.norm(Gp - G) / np.linalg.norm(G))
+            ef.append(np.linalg.norm(Gf - G) / np.linalg.norm(G))
+        out[nb] = (100 * np.median(eg), 100 * np.median(ef))
+    return out
+
+
+def test_offset_sweep_floor():
+    """Figure 1 panel 2: GProj stays at a floor of 0.12-0.17 % at logit std 3 for
+    key offsets from 1 to 1e4, while contracting t directly grows with the offset."""
+    res = _offset_sweep(3.0, [1.0, 100.0, 1e4], rows=256)
+    for nb, (gp, fwd) in res.items():
+        assert 0.12 <= gp <= 0.17, (nb, gp)
+    assert res[1e4][1] > 100 * res[1e4][0]
+    assert res[100.0][1] > 5 * res[100.0][0]
+    assert res[1e4][1] > 20 * res[100.0][1]
