@@ -1,0 +1,162 @@
+/*
+ * gpa.h -- BF16 attention with the GProj gradient correction, for AMD MI355X
+ * (gfx950).  C ABI of libgpa.so.
+ *
+ * The method is "GProj" (gauge projection) from "Broken Symmetry in BF16
+ * Attention: Why FlashAttention Gradients Blow Up Late in Training":
+ *   - the forward is FA3-SBS: the softmax subtracts the unscaled row maximum
+ *     with an explicitly rounded FP32 subtraction before scaling (appendix
+ *     "Implemented Arithmetic and Rounding", eq. gproj-forward);
+ *   - the backward is the native mixed-precision attention backward (BF16
+ *     matrix products, FP32 accumulators) with, in the gproj modes, the rank-one
+ *     correction that restores the zero row sum of the BF16 score-gradient
+ *     operand t after its cast: lambda_i = rho_i / m_i with rho_i = sum_j t_ij
+ *     and m_i = sum_j r_ij, r = BF16(P); dQ = alpha (tK - lambda (rK)) and
+ *     dK = alpha (t^T Q - r^T BF16(lambda Q))  (Section 4; Algorithm 1; eqs.
+ *     gproj-row-mass, gproj-accumulators, gproj-query-implemented,
+ *     gproj-key-implemented).
+ *
+ * Conventions shared by every entry point
+ *   Layout   Q, K, V, O, dO, dQ, dK, dV are [B, H, N, d] contiguous, d innermost,
+ *            BF16 passed as raw 16-bit patterns (uint16_t).  LSE is FP32 [B, H, N].
+ *            Multi-head attention (H query heads = H key/value heads).
+ *   Shapes   B, H, N >= 1; d in {64, 128}; B*H*N*d < 2^31.
+ *   Causal   causal != 0 means query i attends to keys j <= i (square N x N).
+ *   Scale    alpha (the attention scale), finite and > 0; usually 1/sqrt(d).
+ *   Pointers device pointers, 16-byte aligned.  Outputs must not overlap any
+ *            input, any other output or the workspace.
+ *   Stream   a hipStream_t passed as void* (NULL = the null stream).  All work
+ *            is enqueued on it asynchronously; the library never synchronises,
+ *            never allocates or frees device memory, and fully overwrites every
+ *            output.
+ *   Errors   arguments are validated before anything is launched; on error no
+ *            work is enqueued and nothing is written.  GPA_EHIP reports a launch
+ *            failure (text in gpa_last_error(), per thread).  No C++ exception
+ *            crosses this interface.
+ */
+#ifndef GPA_H
+#define GPA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    GPA_OK = 0,
+    GPA_EINVAL = 1,      /* null/misaligned pointer, bad size, scale, mode or aliasing */
+    GPA_ENOTSUP = 2,     /* head dimension other than 64 or 128 */
+    GPA_EWORKSPACE = 3,  /* workspace null or smaller than required */
+    GPA_EHIP = 4         /* a HIP launch failed */
+} gpa_status;
+
+typedef enum {
+    GPA_MODE_PLAIN = 0,   /* FA3-SBS backward: no correction */
+    GPA_MODE_GPROJ_Q = 1, /* query correction only: dQ projected, dK and dV as plain */
+    GPA_MODE_GPROJ = 2    /* query and key corrections: dQ as gproj_q, dK projected */
+} gpa_mode;
+
+/* Library version string, e.g. "gpa 0.1.0 gfx950". */
+const char* gpa_version(void);
+
+/* Text of a status code (static storage). */
+const char* gpa_status_str(gpa_status s);
+
+/* Message of the last error reported on the calling thread ("" if none). */
+const char* gpa_last_error(void);
+
+/*
+ * Forward (FA3-SBS; eq. gproj-forward; Algorithm 1 input state).
+ *   x = Q K^T (unscaled logits, BF16 products, FP32 accumulation), masked;
+ *   z = exp2( fl32[ fl32(x - xmax) * fl32(scale*log2 e) ] ) with xmax the
+ *   running row maximum (the same rule rescales the running sums);
+ *   l = sum z (FP32), O = BF16( sum BF16(z) V / l ), LSE = scale*xmax + ln l.
+ * In : Q, K, V  [B,H,N,d] BF16.
+ * Out: O [B,H,N,d] BF16; LSE [B,H,N] FP32, natural log of the scaled scores.
+ */
+gpa_status gpa_attn_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                        uint16_t* O, float* LSE,
+                        int64_t B, int64_t H, int64_t N, int64_t d,
+                        int causal, float scale, void* stream);
+
+/*
+ * Workspace bytes gpa_attn_bwd needs for this shape and mode (> 0 for valid
+ * shapes, 0 for invalid arguments).  The caller allocates it; its contents on
+ * entry do not matter.
+ */
+size_t gpa_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d, int mode);
+
+/*
+ * Backward (Algorithm 1 with the GProj additions).
+ * In : Q, K, V, O, dO [B,H,N,d] BF16; LSE [B,H,N] FP32 -- O and LSE as written
+ *      by gpa_attn_fwd with the same causal and scale.
+ * Out: dQ, dK, dV [B,H,N,d] BF16.
+ *   D_i   = sum_c fl32(dO_ic O_ic)                         (preprocess)
+ *   P_ij  = exp(scale x_ij - LSE_i) masked, r = BF16(P),
+ *   t_ij  = BF16( fl32[ P_ij (dP_ij - D_i) ] ), dP = dO V^T
+ *   dV    = BF16( r^T dO )                                   (every mode)
+ *   plain   : dQ = BF16(scale * tK),  dK = BF16(scale * t^T Q)
+ *   gproj_q : lambda_i = rho_i / m_i (0 where m_i == 0), rho = rowsum(t),
+ *             m = rowsum(r); dQ = BF16( fl32[scale (tK - lambda rK)] );
+ *             dK, dV bitwise equal to plain
+ *   gproj   : as gproj_q, and dK = BF16( fl32[scale (t^T Q - r^T z)] ),
+ *             z_i = BF16(lambda_i q_i); dQ, dV bitwise equal to gproj_q
+ * All FP32 accumulations are over BF16 products.  The schedule is
+ * deterministic: repeated calls give bitwise identical results.
+ * workspace: device buffer of at least gpa_attn_bwd_workspace_bytes(...)
+ * bytes, 256-byte aligned.  After the call it holds the FP32 row statistics
+ * D, rho, m, lambda at the offsets reported by gpa_bwd_stats_offsets (rho, m
+ * and lambda are zero in plain mode).
+ */
+gpa_status gpa_attn_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                        const uint16_t* O, const float* LSE, const uint16_t* dO,
+                        uint16_t* dQ, uint16_t* dK, uint16_t* dV,
+                        int64_t B, int64_t H, int64_t N, int64_t d,
+                        int causal, float scale, int mode,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Byte offsets, inside the backward workspace, of the FP32 [B,H,N] arrays D
+ * (preprocess row statistic), rho (row mass of t), m (row mass of r) and
+ * lambda = rho/m (Algorithm 1; eq. gproj-row-mass).  Any pointer may be NULL.
+ */
+gpa_status gpa_bwd_stats_offsets(int64_t B, int64_t H, int64_t N, int64_t d, int mode,
+                                 size_t* off_D, size_t* off_rho, size_t* off_m,
+                                 size_t* off_lambda);
+
+/*
+ * FP32 attention baseline (the accuracy class of the paper's "FP32 attention",
+ * appendix on comparison methods: BF16 inputs and outputs, FP32 SIMT
+ * arithmetic, no BF16 or reduced-precision matrix products).  One call runs
+ * forward and backward:
+ * In : Q, K, V, dO [B,H,N,d] BF16.
+ * Out: O, dQ, dK, dV [B,H,N,d] BF16 (RNE casts of FP32 results); LSE [B,H,N] FP32.
+ * The FP32 output (not its BF16 cast) feeds the backward's D = rowsum(dO O).
+ * workspace: at least gpa_fp32_attn_workspace_bytes(...) bytes, 256-byte aligned.
+ */
+size_t gpa_fp32_attn_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d);
+gpa_status gpa_fp32_attn(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                         const uint16_t* dO, uint16_t* O, float* LSE,
+                         uint16_t* dQ, uint16_t* dK, uint16_t* dV,
+                         int64_t B, int64_t H, int64_t N, int64_t d,
+                         int causal, float scale,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Kernel timing for measurement.  While enabled, every kernel the library
+ * launches is bracketed by HIP events on its stream.  gpa_profile_read
+ * synchronises those events, writes per-kernel totals (milliseconds) and launch
+ * counts for kernel ids 0..n-1 (see gpa_kernel_name), clears them, and
+ * returns the number of ids.  Not thread-safe; meant for benchmarks.
+ */
+void gpa_profile_enable(int on);
+int gpa_profile_read(double* total_ms, int64_t* launches, int n);
+const char* gpa_kernel_name(int id);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GPA_H */

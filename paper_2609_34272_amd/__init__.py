@@ -1,0 +1,205 @@
+"""BF16 attention with the GProj gradient correction on AMD MI355X (gfx950).
+
+Thin Python binding of libgpa.so (C ABI in include/gpa.h).  It only marshals
+arguments: it checks tensor properties, allocates outputs and the workspace
+with torch, and passes raw device pointers and the current HIP stream.  Every
+step of the forward and backward runs in the library's HIP kernels; there is no
+fallback path.
+
+Python names mirror the C entry points:
+  gpa_attn_fwd / attn_fwd                 -> O, LSE
+  gpa_attn_bwd / attn_bwd                 -> dQ, dK, dV   (mode plain|gproj_q|gproj)
+  gpa_attn_bwd_workspace_bytes / attn_bwd_workspace_bytes
+  gpa_bwd_stats_offsets / bwd_stats_offsets
+  gpa_fp32_attn / fp32_attn               -> O, LSE, dQ, dK, dV (FP32 baseline)
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch  # noqa: F401  (load torch's HIP runtime first; libgpa binds to it)
+
+__all__ = [
+    "MODES", "lib", "attn_fwd", "attn_bwd", "attn_bwd_workspace_bytes", "bwd_stats_offsets",
+    "fp32_attn", "fp32_attn_workspace_bytes", "profile_enable", "profile_read", "GpaError",
+    "LIB_PATH",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgpa.so")
+MODES = {"plain": 0, "gproj_q": 1, "gproj": 2}
+_STATUS = {0: "GPA_OK", 1: "GPA_EINVAL", 2: "GPA_ENOTSUP", 3: "GPA_EWORKSPACE", 4: "GPA_EHIP"}
+
+_lib = None
+
+
+class GpaError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+def lib():
+    """The loaded libgpa (ctypes).  Builds it in-tree first if it is missing;
+    raises if it cannot be built or loaded."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        from . import build as _build
+        _build.build()
+    L = ctypes.CDLL(LIB_PATH)
+    P, I64, INT, F32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    L.gpa_version.restype = ctypes.c_char_p
+    L.gpa_status_str.restype = ctypes.c_char_p
+    L.gpa_status_str.argtypes = [INT]
+    L.gpa_last_error.restype = ctypes.c_char_p
+    L.gpa_attn_fwd.restype = INT
+    L.gpa_attn_fwd.argtypes = [P, P, P, P, P, I64, I64, I64, I64, INT, F32, P]
+    L.gpa_attn_bwd_workspace_bytes.restype = SZ
+    L.gpa_attn_bwd_workspace_bytes.argtypes = [I64, I64, I64, I64, INT]
+    L.gpa_attn_bwd.restype = INT
+    L.gpa_attn_bwd.argtypes = [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, INT, F32, INT, P, SZ, P]
+    L.gpa_bwd_stats_offsets.restype = INT
+    L.gpa_bwd_stats_offsets.argtypes = [I64, I64, I64, I64, INT] + [ctypes.POINTER(SZ)] * 4
+    L.gpa_fp32_attn_workspace_bytes.restype = SZ
+    L.gpa_fp32_attn_workspace_bytes.argtypes = [I64, I64, I64, I64]
+    L.gpa_fp32_attn.restype = INT
+    L.gpa_fp32_attn.argtypes = [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, INT, F32, P, SZ, P]
+    L.gpa_profile_enable.restype = None
+    L.gpa_profile_enable.argtypes = [INT]
+    L.gpa_profile_read.restype = INT
+    L.gpa_profile_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64), INT]
+    L.gpa_kernel_name.restype = ctypes.c_char_p
+    L.gpa_kernel_name.argtypes = [INT]
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != 0:
+        raise GpaError(status, lib().gpa_last_error().decode())
+
+
+def _stream(t: torch.Tensor) -> int:
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _shape(q: torch.Tensor, name="q"):
+    if q.dim() != 4:
+        raise ValueError(f"{name} must be [B, H, N, d], got {tuple(q.shape)}")
+    return tuple(int(x) for x in q.shape)
+
+
+def _need(t: torch.Tensor, name: str, shape, dtype):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _scale(d: int, scale):
+    return 1.0 / math.sqrt(d) if scale is None else float(scale)
+
+
+def attn_fwd(q, k, v, causal: bool = True, scale=None):
+    """FA3-SBS forward.  q, k, v: bf16 [B, H, N, d] on the GPU.
+    Returns O (bf16, same shape) and LSE (float32 [B, H, N])."""
+    B, H, N, d = _shape(q)
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _need(t, n, (B, H, N, d), torch.bfloat16)
+    o = torch.empty_like(q)
+    lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    _check(lib().gpa_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
+                              B, H, N, d, int(bool(causal)), _scale(d, scale), _stream(q)))
+    return o, lse
+
+
+def attn_bwd_workspace_bytes(B: int, H: int, N: int, d: int, mode="gproj") -> int:
+    return int(lib().gpa_attn_bwd_workspace_bytes(B, H, N, d, MODES[mode] if isinstance(mode, str) else int(mode)))
+
+
+def bwd_stats_offsets(B: int, H: int, N: int, d: int, mode="gproj"):
+    """Byte offsets of D, rho, m, lambda inside the backward workspace."""
+    offs = [ctypes.c_size_t() for _ in range(4)]
+    m = MODES[mode] if isinstance(mode, str) else int(mode)
+    _check(lib().gpa_bwd_stats_offsets(B, H, N, d, m, *[ctypes.byref(o) for o in offs]))
+    return dict(zip(("D", "rho", "m", "lambda"), (o.value for o in offs)))
+
+
+def attn_bwd(q, k, v, o, lse, do, mode: str = "gproj", causal: bool = True, scale=None,
+             workspace=None, return_stats: bool = False):
+    """Backward (plain | gproj_q | gproj).  Returns dQ, dK, dV (bf16); with
+    return_stats=True also a dict of FP32 [B, H, N] tensors D, rho, m, lambda
+    (views into the workspace)."""
+    B, H, N, d = _shape(q)
+    for t, n in ((q, "q"), (k, "k"), (v, "v"), (o, "o"), (do, "do")):
+        _need(t, n, (B, H, N, d), torch.bfloat16)
+    _need(lse, "lse", (B, H, N), torch.float32)
+    mcode = MODES[mode] if isinstance(mode, str) else int(mode)
+    nbytes = int(lib().gpa_attn_bwd_workspace_bytes(B, H, N, d, mcode))
+    if workspace is None:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
+    dq = torch.empty_like(q)
+    dk = torch.empty_like(q)
+    dv = torch.empty_like(q)
+    _check(lib().gpa_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
+                              do.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+                              B, H, N, d, int(bool(causal)), _scale(d, scale), mcode,
+                              workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                              _stream(q)))
+    if not return_stats:
+        return dq, dk, dv
+    offs = bwd_stats_offsets(B, H, N, d, mcode)
+    n = B * H * N
+    stats = {name: workspace[off:off + 4 * n].view(torch.float32).view(B, H, N)
+             for name, off in offs.items()}
+    return dq, dk, dv, stats
+
+
+def fp32_attn_workspace_bytes(B: int, H: int, N: int, d: int) -> int:
+    return int(lib().gpa_fp32_attn_workspace_bytes(B, H, N, d))
+
+
+def fp32_attn(q, k, v, do, causal: bool = True, scale=None):
+    """FP32-arithmetic attention forward + backward with BF16 I/O (baseline).
+    Returns O, LSE, dQ, dK, dV."""
+    B, H, N, d = _shape(q)
+    for t, n in ((q, "q"), (k, "k"), (v, "v"), (do, "do")):
+        _need(t, n, (B, H, N, d), torch.bfloat16)
+    nbytes = fp32_attn_workspace_bytes(B, H, N, d)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
+    o = torch.empty_like(q)
+    lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    _check(lib().gpa_fp32_attn(q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(), o.data_ptr(),
+                               lse.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+                               B, H, N, d, int(bool(causal)), _scale(d, scale), ws.data_ptr(),
+                               nbytes, _stream(q)))
+    return o, lse, dq, dk, dv
+
+
+def profile_enable(on: bool = True):
+    lib().gpa_profile_enable(int(bool(on)))
+
+
+def profile_read():
+    """{kernel name: (total ms, launches)} since the last read; synchronises."""
+    n = 16
+    ms = (ctypes.c_double * n)()
+    cnt = (ctypes.c_int64 * n)()
+    k = lib().gpa_profile_read(ms, cnt, n)
+    return {lib().gpa_kernel_name(i).decode(): (ms[i], cnt[i]) for i in range(k)}
+
+
+# Raw C entry points under their C names (argument marshalling is the caller's).
+def __getattr__(name):
+    if name.startswith("gpa_"):
+        return getattr(lib(), name)
+    raise AttributeError(name)

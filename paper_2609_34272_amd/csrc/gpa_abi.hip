@@ -1,0 +1,298 @@
+// C ABI of libgpa (declared in include/gpa.h): argument validation, workspace
+// layout, kernel sequencing and optional per-kernel timing.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "gpa.h"
+#include "gpa_launch.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+gpa_status fail(gpa_status s, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return s;
+}
+
+struct Buf {
+    const void* p;
+    size_t bytes;
+    const char* name;
+};
+
+bool overlap(const Buf& a, const Buf& b) {
+    const uintptr_t a0 = (uintptr_t)a.p, a1 = a0 + a.bytes;
+    const uintptr_t b0 = (uintptr_t)b.p, b1 = b0 + b.bytes;
+    return a.bytes && b.bytes && a0 < b1 && b0 < a1;
+}
+
+constexpr size_t kAlign = 256;
+size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+gpa_status check_shape(int64_t B, int64_t H, int64_t N, int64_t d, float scale) {
+    if (B < 1 || H < 1 || N < 1)
+        return fail(GPA_EINVAL, "B, H, N must be >= 1 (got %lld, %lld, %lld)", (long long)B,
+                    (long long)H, (long long)N);
+    if (d != 64 && d != 128)
+        return fail(GPA_ENOTSUP, "head dimension %lld not supported (64 or 128)", (long long)d);
+    const double elems = (double)B * (double)H * (double)N * (double)d;
+    if (elems >= 2147483648.0)
+        return fail(GPA_EINVAL, "B*H*N*d = %.0f exceeds 2^31 - 1", elems);
+    if (!std::isfinite(scale) || !(scale > 0.f))
+        return fail(GPA_EINVAL, "scale must be finite and > 0 (got %g)", (double)scale);
+    return GPA_OK;
+}
+
+gpa_status check_ptrs(const std::vector<Buf>& ins, const std::vector<Buf>& outs) {
+    for (const auto* list : {&ins, &outs})
+        for (const Buf& b : *list) {
+            if (!b.p) return fail(GPA_EINVAL, "%s is NULL", b.name);
+            if ((uintptr_t)b.p % 16) return fail(GPA_EINVAL, "%s is not 16-byte aligned", b.name);
+        }
+    for (size_t i = 0; i < outs.size(); ++i) {
+        for (const Buf& b : ins)
+            if (overlap(outs[i], b))
+                return fail(GPA_EINVAL, "%s overlaps %s", outs[i].name, b.name);
+        for (size_t j = i + 1; j < outs.size(); ++j)
+            if (overlap(outs[i], outs[j]))
+                return fail(GPA_EINVAL, "%s overlaps %s", outs[i].name, outs[j].name);
+    }
+    return GPA_OK;
+}
+
+// ---------------------------------------------------------------- timing
+struct ProfRec {
+    int id;
+    hipEvent_t a, b;
+};
+bool g_prof = false;
+std::vector<ProfRec> g_recs;
+std::vector<hipEvent_t> g_pool;
+
+hipEvent_t take_event() {
+    if (!g_pool.empty()) {
+        hipEvent_t e = g_pool.back();
+        g_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+template <class F>
+hipError_t timed(int id, hipStream_t st, F&& launch) {
+    if (!g_prof) return launch();
+    hipEvent_t a = take_event(), b = take_event();
+    if (a) (void)hipEventRecord(a, st);
+    const hipError_t e = launch();
+    if (b) (void)hipEventRecord(b, st);
+    if (a && b) g_recs.push_back({id, a, b});
+    return e;
+}
+
+gpa_status launched(hipError_t e, const char* what) {
+    if (e != hipSuccess) return fail(GPA_EHIP, "%s launch failed: %s", what, hipGetErrorString(e));
+    return GPA_OK;
+}
+
+struct BwdLayout {
+    size_t D, rho, m, lam, total;
+};
+
+BwdLayout bwd_layout(int64_t B, int64_t H, int64_t N) {
+    const size_t row = round_up((size_t)B * H * N * sizeof(float));
+    BwdLayout L;
+    L.D = 0;
+    L.rho = row;
+    L.m = 2 * row;
+    L.lam = 3 * row;
+    L.total = 4 * row;
+    return L;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* gpa_version(void) { return "gpa 0.1.0 gfx950"; }
+
+const char* gpa_status_str(gpa_status s) {
+    switch (s) {
+        case GPA_OK: return "GPA_OK";
+        case GPA_EINVAL: return "GPA_EINVAL: invalid argument";
+        case GPA_ENOTSUP: return "GPA_ENOTSUP: unsupported head dimension";
+        case GPA_EWORKSPACE: return "GPA_EWORKSPACE: workspace missing or too small";
+        case GPA_EHIP: return "GPA_EHIP: HIP launch failure";
+    }
+    return "unknown gpa_status";
+}
+
+const char* gpa_last_error(void) { return g_last_error.c_str(); }
+
+gpa_status gpa_attn_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, uint16_t* O,
+                        float* LSE, int64_t B, int64_t H, int64_t N, int64_t d, int causal,
+                        float scale, void* stream) {
+    gpa_status s = check_shape(B, H, N, d, scale);
+    if (s != GPA_OK) return s;
+    const size_t tb = (size_t)B * H * N * d * 2, lb = (size_t)B * H * N * 4;
+    s = check_ptrs({{Q, tb, "Q"}, {K, tb, "K"}, {V, tb, "V"}}, {{O, tb, "O"}, {LSE, lb, "LSE"}});
+    if (s != GPA_OK) return s;
+    const gpa::Shape sh{(int)(B * H), (int)N, (int)d, causal ? 1 : 0, scale};
+    hipStream_t st = (hipStream_t)stream;
+    return launched(timed(gpa::kKFwd, st, [&] { return gpa::launch_fwd(Q, K, V, O, LSE, sh, st); }),
+                    "fwd_sbs");
+}
+
+size_t gpa_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d, int mode) {
+    if (mode < 0 || mode > 2) return 0;
+    if (B < 1 || H < 1 || N < 1 || (d != 64 && d != 128)) return 0;
+    if ((double)B * H * N * d >= 2147483648.0) return 0;
+    return bwd_layout(B, H, N).total;
+}
+
+gpa_status gpa_bwd_stats_offsets(int64_t B, int64_t H, int64_t N, int64_t d, int mode,
+                                 size_t* off_D, size_t* off_rho, size_t* off_m,
+                                 size_t* off_lambda) {
+    if (gpa_attn_bwd_workspace_bytes(B, H, N, d, mode) == 0)
+        return fail(GPA_EINVAL, "invalid shape or mode");
+    const BwdLayout L = bwd_layout(B, H, N);
+    if (off_D) *off_D = L.D;
+    if (off_rho) *off_rho = L.rho;
+    if (off_m) *off_m = L.m;
+    if (off_lambda) *off_lambda = L.lam;
+    return GPA_OK;
+}
+
+gpa_status gpa_attn_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                        const uint16_t* O, const float* LSE, const uint16_t* dO, uint16_t* dQ,
+                        uint16_t* dK, uint16_t* dV, int64_t B, int64_t H, int64_t N, int64_t d,
+                        int causal, float scale, int mode, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+    gpa_status s = check_shape(B, H, N, d, scale);
+    if (s != GPA_OK) return s;
+    if (mode < 0 || mode > 2) return fail(GPA_EINVAL, "mode %d is not 0, 1 or 2", mode);
+    const size_t need = gpa_attn_bwd_workspace_bytes(B, H, N, d, mode);
+    if (!workspace || workspace_bytes < need)
+        return fail(GPA_EWORKSPACE, "workspace %p of %zu bytes; %zu needed", workspace,
+                    workspace_bytes, need);
+    if ((uintptr_t)workspace % kAlign)
+        return fail(GPA_EWORKSPACE, "workspace is not %zu-byte aligned", kAlign);
+    const size_t tb = (size_t)B * H * N * d * 2, lb = (size_t)B * H * N * 4;
+    s = check_ptrs({{Q, tb, "Q"}, {K, tb, "K"}, {V, tb, "V"}, {O, tb, "O"}, {LSE, lb, "LSE"},
+                    {dO, tb, "dO"}},
+                   {{dQ, tb, "dQ"}, {dK, tb, "dK"}, {dV, tb, "dV"}, {workspace, need, "workspace"}});
+    if (s != GPA_OK) return s;
+
+    const gpa::Shape sh{(int)(B * H), (int)N, (int)d, causal ? 1 : 0, scale};
+    hipStream_t st = (hipStream_t)stream;
+    const BwdLayout L = bwd_layout(B, H, N);
+    char* ws = (char*)workspace;
+    float* Drow = (float*)(ws + L.D);
+    float* rho = (float*)(ws + L.rho);
+    float* msum = (float*)(ws + L.m);
+    float* lam = (float*)(ws + L.lam);
+
+    s = launched(timed(gpa::kKBwdPre, st, [&] { return gpa::launch_bwd_pre(O, dO, Drow, sh, st); }),
+                 "bwd_pre");
+    if (s != GPA_OK) return s;
+    s = launched(timed(gpa::kKBwdDq, st,
+                       [&] {
+                           return gpa::launch_bwd_dq(Q, K, V, dO, LSE, Drow, dQ, rho, msum, lam,
+                                                     mode, sh, st);
+                       }),
+                 "bwd_dq");
+    if (s != GPA_OK) return s;
+    return launched(timed(gpa::kKBwdDkdv, st,
+                          [&] {
+                              return gpa::launch_bwd_dkdv(Q, K, V, dO, LSE, Drow, lam, dK, dV,
+                                                          mode, sh, st);
+                          }),
+                    "bwd_dkdv");
+}
+
+size_t gpa_fp32_attn_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d) {
+    if (B < 1 || H < 1 || N < 1 || (d != 64 && d != 128)) return 0;
+    if ((double)B * H * N * d >= 2147483648.0) return 0;
+    return round_up((size_t)B * H * N * d * 4) + round_up((size_t)B * H * N * 4);
+}
+
+gpa_status gpa_fp32_attn(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                         const uint16_t* dO, uint16_t* O, float* LSE, uint16_t* dQ, uint16_t* dK,
+                         uint16_t* dV, int64_t B, int64_t H, int64_t N, int64_t d, int causal,
+                         float scale, void* workspace, size_t workspace_bytes, void* stream) {
+    gpa_status s = check_shape(B, H, N, d, scale);
+    if (s != GPA_OK) return s;
+    const size_t need = gpa_fp32_attn_workspace_bytes(B, H, N, d);
+    if (!workspace || workspace_bytes < need)
+        return fail(GPA_EWORKSPACE, "workspace %p of %zu bytes; %zu needed", workspace,
+                    workspace_bytes, need);
+    if ((uintptr_t)workspace % kAlign)
+        return fail(GPA_EWORKSPACE, "workspace is not %zu-byte aligned", kAlign);
+    const size_t tb = (size_t)B * H * N * d * 2, lb = (size_t)B * H * N * 4;
+    s = check_ptrs({{Q, tb, "Q"}, {K, tb, "K"}, {V, tb, "V"}, {dO, tb, "dO"}},
+                   {{O, tb, "O"}, {LSE, lb, "LSE"}, {dQ, tb, "dQ"}, {dK, tb, "dK"},
+                    {dV, tb, "dV"}, {workspace, need, "workspace"}});
+    if (s != GPA_OK) return s;
+    const gpa::Shape sh{(int)(B * H), (int)N, (int)d, causal ? 1 : 0, scale};
+    hipStream_t st = (hipStream_t)stream;
+    float* O32 = (float*)workspace;
+    float* Drow = (float*)((char*)workspace + round_up((size_t)B * H * N * d * 4));
+    s = launched(timed(gpa::kKF32Fwd, st,
+                       [&] { return gpa::launch_f32_fwd(Q, K, V, O32, O, LSE, sh, st); }),
+                 "fp32_fwd");
+    if (s != GPA_OK) return s;
+    s = launched(timed(gpa::kKF32Pre, st, [&] { return gpa::launch_f32_pre(O32, dO, Drow, sh, st); }),
+                 "fp32_pre");
+    if (s != GPA_OK) return s;
+    s = launched(timed(gpa::kKF32Dq, st,
+                       [&] { return gpa::launch_f32_dq(Q, K, V, dO, LSE, Drow, dQ, sh, st); }),
+                 "fp32_dq");
+    if (s != GPA_OK) return s;
+    return launched(timed(gpa::kKF32Dkdv, st,
+                          [&] {
+                              return gpa::launch_f32_dkdv(Q, K, V, dO, LSE, Drow, dK, dV, sh, st);
+                          }),
+                    "fp32_dkdv");
+}
+
+void gpa_profile_enable(int on) { g_prof = on != 0; }
+
+int gpa_profile_read(double* total_ms, int64_t* launches, int n) {
+    for (int i = 0; i < n; ++i) {
+        if (total_ms) total_ms[i] = 0.0;
+        if (launches) launches[i] = 0;
+    }
+    for (const ProfRec& r : g_recs) {
+        float ms = 0.f;
+        if (hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess &&
+            r.id < n) {
+            if (total_ms) total_ms[r.id] += ms;
+            if (launches) launches[r.id] += 1;
+        }
+        g_pool.push_back(r.a);
+        g_pool.push_back(r.b);
+    }
+    g_recs.clear();
+    return gpa::kNumKernels;
+}
+
+const char* gpa_kernel_name(int id) {
+    static const char* names[gpa::kNumKernels] = {"fwd_sbs",  "bwd_pre",  "bwd_dq",  "bwd_dkdv",
+                                                  "fp32_fwd", "fp32_pre", "fp32_dq", "fp32_dkdv"};
+    return (id >= 0 && id < gpa::kNumKernels) ? names[id] : "";
+}
+
+}  // extern "C"

@@ -1,0 +1,62 @@
+// Host-side launchers of the libgpa kernels (internal; the public interface is
+// include/gpa.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gpa {
+
+struct Shape {
+    int BH;        // batch * heads
+    int N;         // sequence length
+    int d;         // head dimension (64 or 128)
+    int causal;    // 1: key j visible to query i iff j <= i
+    float scale;   // attention scale alpha
+};
+
+// Kernel ids for timing (gpa_profile_*).
+enum KernelId {
+    kKFwd = 0,
+    kKBwdPre = 1,
+    kKBwdDq = 2,
+    kKBwdDkdv = 3,
+    kKF32Fwd = 4,
+    kKF32Pre = 5,
+    kKF32Dq = 6,
+    kKF32Dkdv = 7,
+    kNumKernels = 8
+};
+
+hipError_t launch_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, uint16_t* O,
+                      float* LSE, const Shape& s, hipStream_t st);
+
+hipError_t launch_bwd_pre(const uint16_t* O, const uint16_t* dO, float* Drow, const Shape& s,
+                          hipStream_t st);
+
+// Query-major pass: t K (and r K, rho, m in the gproj modes), writes dQ and,
+// in the gproj modes, rho, m, lambda.  In plain mode rho, m, lambda are zeroed.
+hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                         const uint16_t* dO, const float* LSE, const float* Drow, uint16_t* dQ,
+                         float* rho, float* msum, float* lambda, int mode, const Shape& s,
+                         hipStream_t st);
+
+// Key-major pass: dV = r^T dO, dK = t^T Q (minus r^T BF16(lambda Q) in gproj mode).
+hipError_t launch_bwd_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                           const uint16_t* dO, const float* LSE, const float* Drow,
+                           const float* lambda, uint16_t* dK, uint16_t* dV, int mode,
+                           const Shape& s, hipStream_t st);
+
+// FP32 baseline.
+hipError_t launch_f32_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, float* O32,
+                          uint16_t* O, float* LSE, const Shape& s, hipStream_t st);
+hipError_t launch_f32_pre(const float* O32, const uint16_t* dO, float* Drow, const Shape& s,
+                          hipStream_t st);
+hipError_t launch_f32_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                         const uint16_t* dO, const float* LSE, const float* Drow, uint16_t* dQ,
+                         const Shape& s, hipStream_t st);
+hipError_t launch_f32_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                           const uint16_t* dO, const float* LSE, const float* Drow,
+                           uint16_t* dK, uint16_t* dV, const Shape& s, hipStream_t st);
+
+}  // namespace gpa
