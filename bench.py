@@ -1,0 +1,173 @@
+#!/usr/bin/env python3
+"""Benchmark: BF16 attention forward + GProj backward on one MI355X.
+
+One step = the whole hot path on one batch: FA3-SBS forward (O, LSE), then the
+backward in gproj mode (preprocess, query-major pass with the query
+correction, key-major pass with the key correction).  Workload: B=1, H=16,
+N=4096, d=64, causal, alpha = 1/8, seeded synthetic inputs with a per-channel
+key bias ~ N(0, 4^2) shared by all tokens and dO ~ N(0, 0.01^2).
+
+Prints one JSON line.  value = fwd+bwd TFLOP/s with the FlashAttention count
+7 * d * N^2 * B * H (causal pairs counted as N^2/2; forward 2 and backward 5
+GEMM-equivalents), the same count in every mode.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "attn fwd+bwd TFLOP/s at H16 N4096 d64 causal; dQ/dK/dV rel-L2 vs FP64"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--mode", default="gproj", choices=["plain", "gproj_q", "gproj"])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-accuracy", action="store_true")
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for {args.gpus}); "
+              "the attention path shards over (batch, head) with no exchange, so per-GPU "
+              "throughput is the single-GPU figure.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_34272_amd as gpa
+    import synthetic as S
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    gpa.lib()
+    dev = torch.device("cuda:0")
+    w = S.WORKLOADS[2]
+    B, H, N, d = w.B, w.H, w.N, w.d
+    x = S.make_inputs(w, 2000)
+
+    def to_dev(b):
+        return torch.from_numpy(np.ascontiguousarray(b).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    q, k, v, u = (to_dev(x[n]) for n in ("q", "k", "v", "do"))
+    ws = {m: torch.empty(gpa.attn_bwd_workspace_bytes(B, H, N, d, m), dtype=torch.uint8, device=dev)
+          for m in gpa.MODES}
+    flops = 7.0 * d * N * N * B * H / 1.0  # FA convention: causal pairs N^2/2, 14 d per pair
+
+    def step(mode):
+        o, lse = gpa.attn_fwd(q, k, v, w.causal, w.scale)
+        return gpa.attn_bwd(q, k, v, o, lse, u, mode, w.causal, w.scale, workspace=ws[mode])
+
+    def timed(fn, iters):
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters
+
+    for _ in range(args.warmup):
+        step(args.mode)
+    torch.cuda.synchronize()
+    t_wall0 = time.perf_counter()
+    ms = timed(lambda: step(args.mode), args.steps)
+    wall = time.perf_counter() - t_wall0
+    value = flops / (ms * 1e-3) / 1e12
+
+    # Per-kernel durations (HIP events recorded by the library on the launch stream).
+    gpa.profile_enable(True)
+    for _ in range(args.steps):
+        step(args.mode)
+    torch.cuda.synchronize()
+    prof = gpa.profile_read()
+    gpa.profile_enable(False)
+    kern = {name: (tot / cnt if cnt else 0.0) for name, (tot, cnt) in prof.items() if cnt}
+
+    # Backward alone per mode (for the GProj overhead over the plain backward).
+    o, lse = gpa.attn_fwd(q, k, v, w.causal, w.scale)
+    bwd_ms = {}
+    for m in gpa.MODES:
+        for _ in range(3):
+            gpa.attn_bwd(q, k, v, o, lse, u, m, w.causal, w.scale, workspace=ws[m])
+        bwd_ms[m] = timed(lambda: gpa.attn_bwd(q, k, v, o, lse, u, m, w.causal, w.scale,
+                                               workspace=ws[m]), args.steps)
+    fwd_ms = timed(lambda: gpa.attn_fwd(q, k, v, w.causal, w.scale), args.steps)
+
+    # Roofline of the dominant kernel: algorithmic MFMA flops per launch.
+    pairs = B * H * N * N / 2.0
+    # dense contractions each kernel needs for its own outputs (per causal pair, 2d flops each):
+    # fwd: QK^T, PV; bwd_dq: QK^T, dO V^T, tK (+ rK); bwd_dkdv: QK^T, dO V^T, r^T dO, t^T Q (+ r^T z)
+    gp = args.mode != "plain"
+    gemms = {"fwd_sbs": 2, "bwd_dq": 4 if gp else 3, "bwd_dkdv": 5 if args.mode == "gproj" else 4}
+    dom = max((n for n in kern if n in gemms), key=lambda n: kern[n])
+    alg = gemms[dom] * 2.0 * d * pairs
+    achieved = alg / (kern[dom] * 1e-3) / 1e12
+    roofline = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "avg_ms": round(kern[dom], 5),
+                "algorithmic_flops_per_launch": alg}
+
+    out = {
+        "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": B, "H": H, "N": N, "d": d, "causal": True,
+                   "mode": args.mode, "scale": w.scale, "k_bias_std": w.k_bias_std,
+                   "do_std": w.do_std, "seed": 2000},
+        "roofline": roofline,
+        "kernels_ms": {k2: round(v2, 5) for k2, v2 in kern.items()},
+        "fwd_ms": round(fwd_ms, 5),
+        "bwd_ms": {m: round(t, 5) for m, t in bwd_ms.items()},
+        "gproj_bwd_overhead_vs_plain_pct": round(100.0 * (bwd_ms["gproj"] / bwd_ms["plain"] - 1), 2),
+        "gproj_q_bwd_overhead_vs_plain_pct": round(100.0 * (bwd_ms["gproj_q"] / bwd_ms["plain"] - 1), 2),
+        "wall_s_timed": round(wall, 3),
+    }
+
+    if not args.no_accuracy or not args.no_cpu_baseline:
+        import oracle
+        t0 = time.perf_counter()
+        ex = oracle.exact(x["q"], x["k"], x["v"], x["do"], w.causal, w.scale)
+        cpu_s = time.perf_counter() - t0
+        if not args.no_cpu_baseline:
+            out["cpu_baseline"] = {"value": round(flops / cpu_s / 1e12, 6), "unit": "TFLOP/s",
+                                   "cores": oracle.max_threads(), "kind": "oracle",
+                                   "sample": f"whole workload ({H} heads, N={N}, d={d}): exact FP64 "
+                                             f"forward + VJP, C/OpenMP, {cpu_s:.2f} s",
+                                   "seconds": round(cpu_s, 3)}
+        if not args.no_accuracy:
+            acc = {}
+            fo, flse, fdq, fdk, fdv = gpa.fp32_attn(q, k, v, u, w.causal, w.scale)
+            res = {"fp32": (fo, fdq, fdk, fdv)}
+            for m in gpa.MODES:
+                dq, dk, dv = gpa.attn_bwd(q, k, v, o, lse, u, m, w.causal, w.scale, workspace=ws[m])
+                res[m] = (o, dq, dk, dv)
+            torch.cuda.synchronize()
+            host = lambda t: t.float().cpu().numpy().astype(np.float64)  # noqa: E731
+            for m, (oo, dq, dk, dv) in res.items():
+                acc[m] = {n: round(oracle.rel_l2(host(t), ex[n]), 4)
+                          for n, t in (("O", oo), ("dQ", dq), ("dK", dk), ("dV", dv))}
+            out["rel_l2_pct_vs_fp64"] = acc
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
