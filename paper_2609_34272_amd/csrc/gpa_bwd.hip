@@ -30,17 +30,15 @@
 // 4*(lane >> 4) + i.  Computing S^T = K Q^T (query-major) or S = Q K^T
 // (key-major) leaves each lane with the probabilities of its own column in
 // exactly the k-layout the next product needs, so P, r and t never pass
-// through LDS.
+// through LDS.  The other operand of that product is read transposed from the
+// row-major LDS tile with the LDS transpose load (ds_read_b64_tr_b16), so every
+// tile is staged once, row-major, with 16-byte writes.
 #include "gpa_device.h"
 #include "gpa_launch.h"
 
 namespace gpa {
 namespace {
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
 // ---------------------------------------------------------------- preprocess
 template <int D>
@@ -68,18 +66,39 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const uint16_t* __restrict
 }
 
 // --------------------------------------------------------- query-major pass
+// P, r, t for one key tile of the query-major pass: lane holds keys 4g+i of
+// each 16-key block for its query.  MASK applies causal and tail masks (only
+// diagonal and tail tiles need them).
+template <bool MASK>
+__device__ __forceinline__ void dq_probs(const f32x4 (&s)[4], const f32x4 (&dp)[4], float c,
+                                         float lse2, float Di, int k0, int g, int qrow, bool qok,
+                                         int N, int causal, bf16x8 (&tf)[2], bf16x8 (&rf)[2]) {
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            float P = fexp2(fmaf(s[kb][i], c, -lse2));
+            if constexpr (MASK) {
+                const int key = k0 + kb * 16 + 4 * g + i;
+                const bool ok = qok && key < N && (!causal || key <= qrow);
+                P = ok ? P : 0.f;
+            }
+            tf[kb >> 1][(kb & 1) * 4 + i] = to_bf16(P * (dp[kb][i] - Di));
+            rf[kb >> 1][(kb & 1) * 4 + i] = to_bf16(P);
+        }
+}
+
 template <int D, bool GPROJ>
-__global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
+__global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
     const float* __restrict__ LSE, const float* __restrict__ Drow, uint16_t* __restrict__ dQ,
     float* __restrict__ rho_out, float* __restrict__ m_out, float* __restrict__ lam_out,
     int BH, int N, int causal, float scale) {
     constexpr int RP = Pitch<D>::row;
-    constexpr int TP = Pitch<D>::tr;
+    constexpr int CH = kTile * D / 8 / kThreads;  // 16-byte chunks per thread per tile
     __shared__ __attribute__((aligned(16))) uint16_t Ks[kTile * RP];  // K row-major
     __shared__ __attribute__((aligned(16))) uint16_t Vs[kTile * RP];  // V row-major
-    __shared__ __attribute__((aligned(16))) uint16_t Kt[D * TP];      // K transposed
 
     const int T = (N + kTile - 1) / kTile;
     int bh, tile;
@@ -90,52 +109,55 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
     const int g = lane >> 4, c16 = lane & 15;
     const int qrow = tile * kTile + wave * 16 + c16;
     const bool qok = qrow < N;
-    const size_t ridx = (size_t)bh * N + qrow;
+    const int qcl = qok ? qrow : N - 1;
+    const size_t ridx = (size_t)bh * N + qcl;
 
     bf16x8 qf[D / 32], uf[D / 32];
 #pragma unroll
     for (int kc = 0; kc < D / 32; ++kc) {
-        u32x4 wq = {0u, 0u, 0u, 0u}, wu = {0u, 0u, 0u, 0u};
-        if (qok) {
-            wq = *reinterpret_cast<const u32x4*>(Q + hoff + (size_t)qrow * D + kc * 32 + 8 * g);
-            wu = *reinterpret_cast<const u32x4*>(dO + hoff + (size_t)qrow * D + kc * 32 + 8 * g);
-        }
-        qf[kc] = __builtin_bit_cast(bf16x8, wq);
-        uf[kc] = __builtin_bit_cast(bf16x8, wu);
+        qf[kc] = __builtin_bit_cast(bf16x8, ld_row16(Q + hoff, qrow, N, D, kc * 32 + 8 * g));
+        uf[kc] = __builtin_bit_cast(bf16x8, ld_row16(dO + hoff, qrow, N, D, kc * 32 + 8 * g));
     }
     const float c = scale * kLog2e;
-    const float lse2 = qok ? LSE[ridx] * kLog2e : 0.f;
-    const float Di = qok ? Drow[ridx] : 0.f;
+    const float lse2 = LSE[ridx] * kLog2e;
+    const float Di = Drow[ridx];
+    const bf16x8 ones = ones_row0(c16);
 
     f32x4 accA[D / 16], accB[GPROJ ? D / 16 : 1];
 #pragma unroll
     for (int mb = 0; mb < D / 16; ++mb) accA[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int mb = 0; mb < (GPROJ ? D / 16 : 1); ++mb) accB[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float rho = 0.f, msum = 0.f;
+    f32x4 accR = {0.f, 0.f, 0.f, 0.f}, accM = {0.f, 0.f, 0.f, 0.f};
 
     const int nkv = causal ? min(T, tile + 1) : T;
+    const bool q_tail = tile * kTile + kTile > N;
+
+    u32x4 kreg[CH], vreg[CH];
+    auto fetch = [&](int k0) {
+#pragma unroll
+        for (int cI = 0; cI < CH; ++cI) {
+            const int ch = tid + cI * kThreads;
+            const int r = ch / (D / 8);
+            const int cc = (ch - r * (D / 8)) * 8;
+            kreg[cI] = ld_row16(K + hoff, k0 + r, N, D, cc);
+            vreg[cI] = ld_row16(V + hoff, k0 + r, N, D, cc);
+        }
+    };
+    fetch(0);
     for (int kt = 0; kt < nkv; ++kt) {
         const int k0 = kt * kTile;
         __syncthreads();
-        for (int ch = tid; ch < kTile * D / 8; ch += kThreads) {
+#pragma unroll
+        for (int cI = 0; cI < CH; ++cI) {
+            const int ch = tid + cI * kThreads;
             const int r = ch / (D / 8);
             const int cc = (ch - r * (D / 8)) * 8;
-            const int row = k0 + r;
-            u32x4 kw = {0u, 0u, 0u, 0u}, vw = {0u, 0u, 0u, 0u};
-            if (row < N) {
-                kw = *reinterpret_cast<const u32x4*>(K + hoff + (size_t)row * D + cc);
-                vw = *reinterpret_cast<const u32x4*>(V + hoff + (size_t)row * D + cc);
-            }
-            *reinterpret_cast<u32x4*>(Ks + r * RP + cc) = kw;
-            *reinterpret_cast<u32x4*>(Vs + r * RP + cc) = vw;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                Kt[(cc + 2 * e) * TP + r] = (uint16_t)(kw[e] & 0xFFFFu);
-                Kt[(cc + 2 * e + 1) * TP + r] = (uint16_t)(kw[e] >> 16);
-            }
+            *reinterpret_cast<u32x4*>(Ks + r * RP + cc) = kreg[cI];
+            *reinterpret_cast<u32x4*>(Vs + r * RP + cc) = vreg[cI];
         }
         __syncthreads();
+        if (kt + 1 < nkv) fetch(k0 + kTile);
 
         // S^T = K Q^T and dP^T = V dO^T: lane holds keys 4g+i of each 16-key
         // block for its own query.
@@ -153,38 +175,34 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
             }
         }
         bf16x8 tf[2], rf[2];
+        const bool edge = (causal && kt == tile) || q_tail || k0 + kTile > N;
+        if (edge)
+            dq_probs<true>(s, dp, c, lse2, Di, k0, g, qrow, qok, N, causal, tf, rf);
+        else
+            dq_probs<false>(s, dp, c, lse2, Di, k0, g, qrow, qok, N, causal, tf, rf);
+
+        // A^T[d][query] += K^T[d][key] t^T[key][query]  (and B^T with r); the
+        // row sums rho, m come from a constant ones operand.
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
+        for (int kc2 = 0; kc2 < 2; ++kc2) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int key = k0 + kb * 16 + 4 * g + i;
-                const bool ok = qok && key < N && (!causal || key <= qrow);
-                const float P = ok ? fexp2(fmaf(s[kb][i], c, -lse2)) : 0.f;
-                const __bf16 rb = to_bf16(P);
-                const __bf16 tb = to_bf16(P * (dp[kb][i] - Di));
-                if (GPROJ) {
-                    rho += bf16_to_f32(tb);
-                    msum += bf16_to_f32(rb);
-                }
-                tf[kb >> 1][(kb & 1) * 4 + i] = tb;
-                rf[kb >> 1][(kb & 1) * 4 + i] = rb;
-            }
-        // A^T[d][query] += K^T[d][key] t^T[key][query]  (and B^T with r).
-#pragma unroll
-        for (int mb = 0; mb < D / 16; ++mb)
-#pragma unroll
-            for (int kc2 = 0; kc2 < 2; ++kc2) {
-                const uint16_t* a = Kt + (mb * 16 + c16) * TP + kc2 * 32 + 4 * g;
-                const bf16x8 ka = ld_b64x2(a, a + 16);
+            for (int mb = 0; mb < D / 16; ++mb) {
+                const bf16x8 ka = ld_tr_operand(Ks, RP, kc2 * 32, mb * 16, c16, g);
                 accA[mb] = mfma_16x16x32(ka, tf[kc2], accA[mb]);
                 if (GPROJ) accB[mb] = mfma_16x16x32(ka, rf[kc2], accB[mb]);
             }
+            if (GPROJ) {
+                accR = mfma_16x16x32(ones, tf[kc2], accR);
+                accM = mfma_16x16x32(ones, rf[kc2], accM);
+            }
+        }
     }
 
-    float lam = 0.f;
+    // rho and m of this lane's query sit in accumulator row 0 (lanes g == 0).
+    float lam = 0.f, rho = 0.f, msum = 0.f;
     if (GPROJ) {
-        rho = xor_sum(rho);
-        msum = xor_sum(msum);
+        rho = __shfl(accR[0], c16);
+        msum = __shfl(accM[0], c16);
         lam = (msum != 0.f) ? rho / msum : 0.f;  // one IEEE FP32 division
     }
     if (qok) {
@@ -206,35 +224,56 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
             st_bf16x4(drow + mb * 16 + 4 * g, v[0], v[1], v[2], v[3]);
         }
         if (g == 0) {
-            rho_out[ridx] = GPROJ ? rho : 0.f;
-            m_out[ridx] = GPROJ ? msum : 0.f;
+            rho_out[ridx] = rho;
+            m_out[ridx] = msum;
             lam_out[ridx] = lam;
         }
     }
 }
 
 // ----------------------------------------------------------- key-major pass
+// P, r, t for one query tile of the key-major pass: lane holds queries 4g+i of
+// each 16-query block for its key.
+template <bool MASK>
+__device__ __forceinline__ void dkdv_probs(const f32x4 (&s)[4], const f32x4 (&dp)[4],
+                                           const f32x4 (&l2)[4], const f32x4 (&dd)[4], float c,
+                                           int q0, int g, int krow, int N, int causal,
+                                           bf16x8 (&tf)[2], bf16x8 (&rf)[2]) {
+#pragma unroll
+    for (int mq = 0; mq < 4; ++mq)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            float P = fexp2(fmaf(s[mq][i], c, -l2[mq][i]));
+            if constexpr (MASK) {
+                const int query = q0 + mq * 16 + 4 * g + i;
+                const bool ok = krow < N && query < N && (!causal || krow <= query);
+                P = ok ? P : 0.f;
+            }
+            tf[mq >> 1][(mq & 1) * 4 + i] = to_bf16(P * (dp[mq][i] - dd[mq][i]));
+            rf[mq >> 1][(mq & 1) * 4 + i] = to_bf16(P);
+        }
+}
+
 template <int D, bool GPROJ>
-__global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
+__global__ __launch_bounds__(kThreads, D == 64 ? 2 : 1) void bwd_dkdv_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
     const float* __restrict__ LSE, const float* __restrict__ Drow,
     const float* __restrict__ lam, uint16_t* __restrict__ dK, uint16_t* __restrict__ dV,
     int BH, int N, int causal, float scale) {
     constexpr int RP = Pitch<D>::row;
-    constexpr int TP = Pitch<D>::tr;
+    constexpr int CH = kTile * D / 8 / kThreads;
     __shared__ __attribute__((aligned(16))) uint16_t Qs[kTile * RP];   // Q row-major
     __shared__ __attribute__((aligned(16))) uint16_t Us[kTile * RP];   // dO row-major
-    __shared__ __attribute__((aligned(16))) uint16_t Qt[D * TP];       // Q transposed
-    __shared__ __attribute__((aligned(16))) uint16_t Ut[D * TP];       // dO transposed
-    __shared__ __attribute__((aligned(16))) uint16_t Zt[GPROJ ? D * TP : 8];  // BF16(lambda q)^T
-    __shared__ float lse2s[kTile];
-    __shared__ float Ds[kTile];
+    __shared__ __attribute__((aligned(16))) uint16_t Zs[GPROJ ? kTile * RP : 8];  // BF16(lambda q)
+    __shared__ __attribute__((aligned(16))) float lse2s[kTile];
+    __shared__ __attribute__((aligned(16))) float Ds[kTile];
 
     const int T = (N + kTile - 1) / kTile;
     int bh, tile;
     map_block(blockIdx.x, BH, T, false, &bh, &tile);
     const size_t hoff = (size_t)bh * N * D;
+    const size_t soff = (size_t)bh * N;
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
@@ -245,13 +284,8 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
     bf16x8 kf[D / 32], vf[D / 32];
 #pragma unroll
     for (int kc = 0; kc < D / 32; ++kc) {
-        u32x4 wk = {0u, 0u, 0u, 0u}, wv = {0u, 0u, 0u, 0u};
-        if (kok) {
-            wk = *reinterpret_cast<const u32x4*>(K + hoff + (size_t)krow * D + kc * 32 + 8 * g);
-            wv = *reinterpret_cast<const u32x4*>(V + hoff + (size_t)krow * D + kc * 32 + 8 * g);
-        }
-        kf[kc] = __builtin_bit_cast(bf16x8, wk);
-        vf[kc] = __builtin_bit_cast(bf16x8, wv);
+        kf[kc] = __builtin_bit_cast(bf16x8, ld_row16(K + hoff, krow, N, D, kc * 32 + 8 * g));
+        vf[kc] = __builtin_bit_cast(bf16x8, ld_row16(V + hoff, krow, N, D, kc * 32 + 8 * g));
     }
     const float c = scale * kLog2e;
 
@@ -265,42 +299,55 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
     for (int mb = 0; mb < (GPROJ ? D / 16 : 1); ++mb) accC[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     const int qt0 = causal ? tile : 0;
+    const bool k_tail = tile * kTile + kTile > N;
+
+    u32x4 qreg[CH], ureg[CH];
+    float lreg[CH];
+    float lse_reg = 0.f, d_reg = 0.f;
+    auto fetch = [&](int q0) {
+#pragma unroll
+        for (int cI = 0; cI < CH; ++cI) {
+            const int ch = tid + cI * kThreads;
+            const int r = ch / (D / 8);
+            const int cc = (ch - r * (D / 8)) * 8;
+            qreg[cI] = ld_row16(Q + hoff, q0 + r, N, D, cc);
+            ureg[cI] = ld_row16(dO + hoff, q0 + r, N, D, cc);
+            if (GPROJ) lreg[cI] = lam[soff + min(q0 + r, N - 1)];
+        }
+        if (tid < kTile) {
+            const int row = min(q0 + tid, N - 1);
+            lse_reg = LSE[soff + row];
+            d_reg = Drow[soff + row];
+        }
+    };
+    fetch(qt0 * kTile);
     for (int qt = qt0; qt < T; ++qt) {
         const int q0 = qt * kTile;
         __syncthreads();
-        for (int ch = tid; ch < kTile * D / 8; ch += kThreads) {
+#pragma unroll
+        for (int cI = 0; cI < CH; ++cI) {
+            const int ch = tid + cI * kThreads;
             const int r = ch / (D / 8);
             const int cc = (ch - r * (D / 8)) * 8;
-            const int row = q0 + r;
-            u32x4 qw = {0u, 0u, 0u, 0u}, uw = {0u, 0u, 0u, 0u};
-            float lr = 0.f;
-            if (row < N) {
-                qw = *reinterpret_cast<const u32x4*>(Q + hoff + (size_t)row * D + cc);
-                uw = *reinterpret_cast<const u32x4*>(dO + hoff + (size_t)row * D + cc);
-                if (GPROJ) lr = lam[(size_t)bh * N + row];
-            }
+            const u32x4 qw = qreg[cI];
             *reinterpret_cast<u32x4*>(Qs + r * RP + cc) = qw;
-            *reinterpret_cast<u32x4*>(Us + r * RP + cc) = uw;
+            *reinterpret_cast<u32x4*>(Us + r * RP + cc) = ureg[cI];
+            if (GPROJ) {
+                // z = BF16(fl32(lambda q))
+                u32x4 zw;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                Qt[(cc + 2 * e) * TP + r] = (uint16_t)(qw[e] & 0xFFFFu);
-                Qt[(cc + 2 * e + 1) * TP + r] = (uint16_t)(qw[e] >> 16);
-                Ut[(cc + 2 * e) * TP + r] = (uint16_t)(uw[e] & 0xFFFFu);
-                Ut[(cc + 2 * e + 1) * TP + r] = (uint16_t)(uw[e] >> 16);
-                if (GPROJ) {
-                    // z = BF16(fl32(lambda q))
-                    Zt[(cc + 2 * e) * TP + r] = bf16_bits(lr * lo_bf16(qw[e]));
-                    Zt[(cc + 2 * e + 1) * TP + r] = bf16_bits(lr * hi_bf16(qw[e]));
-                }
+                for (int e = 0; e < 4; ++e)
+                    zw[e] = (uint32_t)bf16_bits(lreg[cI] * lo_bf16(qw[e])) |
+                            ((uint32_t)bf16_bits(lreg[cI] * hi_bf16(qw[e])) << 16);
+                *reinterpret_cast<u32x4*>(Zs + r * RP + cc) = zw;
             }
         }
         if (tid < kTile) {
-            const int row = q0 + tid;
-            const size_t ri = (size_t)bh * N + row;
-            lse2s[tid] = row < N ? LSE[ri] * kLog2e : 0.f;
-            Ds[tid] = row < N ? Drow[ri] : 0.f;
+            lse2s[tid] = lse_reg * kLog2e;
+            Ds[tid] = d_reg;
         }
         __syncthreads();
+        if (qt + 1 < T) fetch(q0 + kTile);
 
         // S = Q K^T and dP = dO V^T: lane holds queries 4g+i of each 16-query
         // block for its own key.
@@ -317,28 +364,31 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
                                        vf[kc], dp[mq]);
             }
         }
+        f32x4 l2[4], dd[4];
+#pragma unroll
+        for (int mq = 0; mq < 4; ++mq) {
+            l2[mq] = *reinterpret_cast<const f32x4*>(lse2s + mq * 16 + 4 * g);
+            dd[mq] = *reinterpret_cast<const f32x4*>(Ds + mq * 16 + 4 * g);
+        }
         bf16x8 tf[2], rf[2];
-#pragma unroll
-        for (int mq = 0; mq < 4; ++mq)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int ql = mq * 16 + 4 * g + i;
-                const int query = q0 + ql;
-                const bool ok = kok && query < N && (!causal || krow <= query);
-                const float P = ok ? fexp2(fmaf(s[mq][i], c, -lse2s[ql])) : 0.f;
-                tf[mq >> 1][(mq & 1) * 4 + i] = to_bf16(P * (dp[mq][i] - Ds[ql]));
-                rf[mq >> 1][(mq & 1) * 4 + i] = to_bf16(P);
-            }
+        const bool edge = (causal && qt == tile) || k_tail || q0 + kTile > N;
+        if (edge)
+            dkdv_probs<true>(s, dp, l2, dd, c, q0, g, krow, N, causal, tf, rf);
+        else
+            dkdv_probs<false>(s, dp, l2, dd, c, q0, g, krow, N, causal, tf, rf);
+
         // dV^T[dv][key] += dO^T r ; dK^T += Q^T t ; C^T += Z^T r.
 #pragma unroll
         for (int mb = 0; mb < D / 16; ++mb)
 #pragma unroll
             for (int kc2 = 0; kc2 < 2; ++kc2) {
-                const int off = (mb * 16 + c16) * TP + kc2 * 32 + 4 * g;
-                accV[mb] = mfma_16x16x32(ld_b64x2(Ut + off, Ut + off + 16), rf[kc2], accV[mb]);
-                accK[mb] = mfma_16x16x32(ld_b64x2(Qt + off, Qt + off + 16), tf[kc2], accK[mb]);
+                accV[mb] = mfma_16x16x32(ld_tr_operand(Us, RP, kc2 * 32, mb * 16, c16, g), rf[kc2],
+                                         accV[mb]);
+                accK[mb] = mfma_16x16x32(ld_tr_operand(Qs, RP, kc2 * 32, mb * 16, c16, g), tf[kc2],
+                                         accK[mb]);
                 if (GPROJ)
-                    accC[mb] = mfma_16x16x32(ld_b64x2(Zt + off, Zt + off + 16), rf[kc2], accC[mb]);
+                    accC[mb] = mfma_16x16x32(ld_tr_operand(Zs, RP, kc2 * 32, mb * 16, c16, g),
+                                             rf[kc2], accC[mb]);
             }
     }
 

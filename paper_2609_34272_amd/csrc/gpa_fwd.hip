@@ -5,8 +5,8 @@
 // exp2(0) = 1.
 //
 // Schedule: one workgroup per (batch*head, 64-query tile); 4 waves, each owning
-// 16 queries.  K and V tiles of 64 keys are staged in LDS (K row-major, V
-// transposed).  A wave computes S^T = K Q^T with v_mfma_f32_16x16x32_bf16, so
+// 16 queries.  K and V tiles of 64 keys are staged row-major in LDS (V is read
+// back transposed with the LDS transpose load).  A wave computes S^T = K Q^T with v_mfma_f32_16x16x32_bf16, so
 // each lane holds 16 logits of ONE query (its column): the row maximum and the
 // row sum are in-lane except for a 4-way exchange.  The probabilities are then
 // already in the B-operand layout of O^T += V^T P^T, whose accumulator again
@@ -17,17 +17,15 @@
 namespace gpa {
 namespace {
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
 template <int D>
-__global__ __launch_bounds__(kThreads) void fwd_sbs_kernel(
+__global__ __launch_bounds__(kThreads, 2) void fwd_sbs_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, uint16_t* __restrict__ O, float* __restrict__ LSE,
     int BH, int N, int causal, float scale) {
     constexpr int RP = Pitch<D>::row;
-    constexpr int TP = Pitch<D>::tr;
+    constexpr int CH = kTile * D / 8 / kThreads;
     __shared__ __attribute__((aligned(16))) uint16_t Ks[kTile * RP];
-    __shared__ __attribute__((aligned(16))) uint16_t Vt[D * TP];
+    __shared__ __attribute__((aligned(16))) uint16_t Vs[kTile * RP];
 
     const int T = (N + kTile - 1) / kTile;
     int bh, tile;
@@ -42,11 +40,8 @@ __global__ __launch_bounds__(kThreads) void fwd_sbs_kernel(
     // Q^T as the B operand: column = this lane's query, k = d.
     bf16x8 qf[D / 32];
 #pragma unroll
-    for (int kc = 0; kc < D / 32; ++kc) {
-        u32x4 w = {0u, 0u, 0u, 0u};
-        if (qok) w = *reinterpret_cast<const u32x4*>(Q + hoff + (size_t)qrow * D + kc * 32 + 8 * g);
-        qf[kc] = __builtin_bit_cast(bf16x8, w);
-    }
+    for (int kc = 0; kc < D / 32; ++kc)
+        qf[kc] = __builtin_bit_cast(bf16x8, ld_row16(Q + hoff, qrow, N, D, kc * 32 + 8 * g));
 
     const float c = scale * kLog2e;  // fl32(alpha log2 e)
     float mrun = -INFINITY;          // running maximum of the unscaled logits
@@ -57,26 +52,32 @@ __global__ __launch_bounds__(kThreads) void fwd_sbs_kernel(
 
     const int kv_end = causal ? min(N, (tile + 1) * kTile) : N;
     const int nkv = (kv_end + kTile - 1) / kTile;
+
+    u32x4 kreg[CH], vreg[CH];
+    auto fetch = [&](int k0) {
+#pragma unroll
+        for (int cI = 0; cI < CH; ++cI) {
+            const int ch = tid + cI * kThreads;
+            const int r = ch / (D / 8);
+            const int cc = (ch - r * (D / 8)) * 8;
+            kreg[cI] = ld_row16(K + hoff, k0 + r, N, D, cc);
+            vreg[cI] = ld_row16(V + hoff, k0 + r, N, D, cc);
+        }
+    };
+    fetch(0);
     for (int kt = 0; kt < nkv; ++kt) {
         const int k0 = kt * kTile;
         __syncthreads();
-        for (int ch = tid; ch < kTile * D / 8; ch += kThreads) {
+#pragma unroll
+        for (int cI = 0; cI < CH; ++cI) {
+            const int ch = tid + cI * kThreads;
             const int r = ch / (D / 8);
             const int cc = (ch - r * (D / 8)) * 8;
-            const int row = k0 + r;
-            u32x4 kw = {0u, 0u, 0u, 0u}, vw = {0u, 0u, 0u, 0u};
-            if (row < N) {
-                kw = *reinterpret_cast<const u32x4*>(K + hoff + (size_t)row * D + cc);
-                vw = *reinterpret_cast<const u32x4*>(V + hoff + (size_t)row * D + cc);
-            }
-            *reinterpret_cast<u32x4*>(Ks + r * RP + cc) = kw;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                Vt[(cc + 2 * e) * TP + r] = (uint16_t)(vw[e] & 0xFFFFu);
-                Vt[(cc + 2 * e + 1) * TP + r] = (uint16_t)(vw[e] >> 16);
-            }
+            *reinterpret_cast<u32x4*>(Ks + r * RP + cc) = kreg[cI];
+            *reinterpret_cast<u32x4*>(Vs + r * RP + cc) = vreg[cI];
         }
         __syncthreads();
+        if (kt + 1 < nkv) fetch(k0 + kTile);
 
         // S^T[key][query] for 4 blocks of 16 keys.
         f32x4 s[4];
@@ -88,21 +89,27 @@ __global__ __launch_bounds__(kThreads) void fwd_sbs_kernel(
                 s[kb] = mfma_16x16x32(ld_b128(Ks + (kb * 16 + c16) * RP + kc * 32 + 8 * g), qf[kc],
                                       s[kb]);
         }
-        float mx = -INFINITY;
+        // Only the diagonal tile and the key tail need masks (uniform branch).
+        if ((causal && kt == tile) || k0 + kTile > N) {
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int key = k0 + kb * 16 + 4 * g + i;
+                    const bool ok = key < N && (!causal || key <= qrow);
+                    s[kb][i] = ok ? s[kb][i] : -INFINITY;
+                }
+        }
+        float mx = s[0][0];
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int key = k0 + kb * 16 + 4 * g + i;
-                const bool ok = key < N && (!causal || key <= qrow);
-                const float x = ok ? s[kb][i] : -INFINITY;
-                s[kb][i] = x;
-                mx = fmaxf(mx, x);
-            }
+            for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[kb][i]);
         mx = xor_max(mx);
         const float mnew = fmaxf(mrun, mx);
         // Rescale by exp2(fl32[fl32(mold - mnew) * c]): the same rule as z.
-        const float corr = (mnew == -INFINITY) ? 1.f : fexp2((mrun - mnew) * c);
+        // (mnew is finite: key 0 is visible to every row in tile 0.)
+        const float corr = fexp2((mrun - mnew) * c);
         lrun *= corr;
 #pragma unroll
         for (int mb = 0; mb < D / 16; ++mb) acc[mb] *= corr;
@@ -122,10 +129,9 @@ __global__ __launch_bounds__(kThreads) void fwd_sbs_kernel(
 #pragma unroll
         for (int mb = 0; mb < D / 16; ++mb)
 #pragma unroll
-            for (int kc2 = 0; kc2 < 2; ++kc2) {
-                const uint16_t* a = Vt + (mb * 16 + c16) * TP + kc2 * 32 + 4 * g;
-                acc[mb] = mfma_16x16x32(ld_b64x2(a, a + 16), pf[kc2], acc[mb]);
-            }
+            for (int kc2 = 0; kc2 < 2; ++kc2)
+                acc[mb] = mfma_16x16x32(ld_tr_operand(Vs, RP, kc2 * 32, mb * 16, c16, g), pf[kc2],
+                                        acc[mb]);
     }
 
     const float ltot = xor_sum(lrun);
