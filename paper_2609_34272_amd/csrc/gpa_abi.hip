@@ -109,17 +109,20 @@ gpa_status launched(hipError_t e, const char* what) {
 }
 
 struct BwdLayout {
-    size_t D, rho, m, lam, total;
+    size_t D, rho, m, lam, z, total;
 };
 
-BwdLayout bwd_layout(int64_t B, int64_t H, int64_t N) {
+// Four FP32 [B,H,N] row statistics, then (gproj mode only) the BF16
+// [B,H,N,d] tensor z = BF16(lambda q) that the key correction contracts.
+BwdLayout bwd_layout(int64_t B, int64_t H, int64_t N, int64_t d, int mode) {
     const size_t row = round_up((size_t)B * H * N * sizeof(float));
     BwdLayout L;
     L.D = 0;
     L.rho = row;
     L.m = 2 * row;
     L.lam = 3 * row;
-    L.total = 4 * row;
+    L.z = 4 * row;
+    L.total = L.z + (mode == 2 ? round_up((size_t)B * H * N * d * 2) : 0);
     return L;
 }
 
@@ -160,7 +163,7 @@ size_t gpa_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d, 
     if (mode < 0 || mode > 2) return 0;
     if (B < 1 || H < 1 || N < 1 || (d != 64 && d != 128)) return 0;
     if ((double)B * H * N * d >= 2147483648.0) return 0;
-    return bwd_layout(B, H, N).total;
+    return bwd_layout(B, H, N, d, mode).total;
 }
 
 gpa_status gpa_bwd_stats_offsets(int64_t B, int64_t H, int64_t N, int64_t d, int mode,
@@ -168,7 +171,7 @@ gpa_status gpa_bwd_stats_offsets(int64_t B, int64_t H, int64_t N, int64_t d, int
                                  size_t* off_lambda) {
     if (gpa_attn_bwd_workspace_bytes(B, H, N, d, mode) == 0)
         return fail(GPA_EINVAL, "invalid shape or mode");
-    const BwdLayout L = bwd_layout(B, H, N);
+    const BwdLayout L = bwd_layout(B, H, N, d, mode);
     if (off_D) *off_D = L.D;
     if (off_rho) *off_rho = L.rho;
     if (off_m) *off_m = L.m;
@@ -198,26 +201,24 @@ gpa_status gpa_attn_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
 
     const gpa::Shape sh{(int)(B * H), (int)N, (int)d, causal ? 1 : 0, scale};
     hipStream_t st = (hipStream_t)stream;
-    const BwdLayout L = bwd_layout(B, H, N);
+    const BwdLayout L = bwd_layout(B, H, N, d, mode);
     char* ws = (char*)workspace;
     float* Drow = (float*)(ws + L.D);
     float* rho = (float*)(ws + L.rho);
     float* msum = (float*)(ws + L.m);
     float* lam = (float*)(ws + L.lam);
+    uint16_t* zbuf = mode == 2 ? (uint16_t*)(ws + L.z) : nullptr;
 
-    s = launched(timed(gpa::kKBwdPre, st, [&] { return gpa::launch_bwd_pre(O, dO, Drow, sh, st); }),
-                 "bwd_pre");
-    if (s != GPA_OK) return s;
     s = launched(timed(gpa::kKBwdDq, st,
                        [&] {
-                           return gpa::launch_bwd_dq(Q, K, V, dO, LSE, Drow, dQ, rho, msum, lam,
-                                                     mode, sh, st);
+                           return gpa::launch_bwd_dq(Q, K, V, O, dO, LSE, Drow, dQ, rho, msum,
+                                                     lam, zbuf, mode, sh, st);
                        }),
                  "bwd_dq");
     if (s != GPA_OK) return s;
     return launched(timed(gpa::kKBwdDkdv, st,
                           [&] {
-                              return gpa::launch_bwd_dkdv(Q, K, V, dO, LSE, Drow, lam, dK, dV,
+                              return gpa::launch_bwd_dkdv(Q, K, V, dO, LSE, Drow, zbuf, dK, dV,
                                                           mode, sh, st);
                           }),
                     "bwd_dkdv");
@@ -290,8 +291,8 @@ int gpa_profile_read(double* total_ms, int64_t* launches, int n) {
 }
 
 const char* gpa_kernel_name(int id) {
-    static const char* names[gpa::kNumKernels] = {"fwd_sbs",  "bwd_pre",  "bwd_dq",  "bwd_dkdv",
-                                                  "fp32_fwd", "fp32_pre", "fp32_dq", "fp32_dkdv"};
+    static const char* names[gpa::kNumKernels] = {"fwd_sbs",  "bwd_dq",   "bwd_dkdv", "fp32_fwd",
+                                                  "fp32_pre", "fp32_dq", "fp32_dkdv"};
     return (id >= 0 && id < gpa::kNumKernels) ? names[id] : "";
 }
 

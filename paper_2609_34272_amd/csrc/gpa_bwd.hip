@@ -7,16 +7,16 @@
 // with atomic adds from a key-major loop and then needs a second key-major pass
 // for dK, because lambda_i = rho_i / m_i is known only after row i has seen
 // every key.  Here the same arithmetic is split by ownership instead:
-//   1. bwd_pre   : D_i = rowsum(dO_i * O_i) in FP32.
-//   2. bwd_dq    : query-major.  A workgroup owns 64 query rows and streams the
+//   1. bwd_dq    : query-major.  A workgroup owns 64 query rows and streams the
 //                  key tiles, so A = tK, B = rK, rho and m stay in registers; at
 //                  the end it forms lambda = rho/m once and writes
 //                  dQ = BF16(fl32[alpha (A - lambda B)]) and lambda.
-//   3. bwd_dkdv  : key-major.  A workgroup owns 64 keys and streams the query
-//                  tiles; with lambda already known it accumulates dV = r^T dO,
-//                  dK^acc = t^T Q and C = r^T z (z = BF16(lambda q), formed while
-//                  the query tile is staged) and writes
-//                  dK = BF16(fl32[alpha (dK^acc - C)]).
+//                  In gproj mode it also writes z = BF16(lambda q), once per row.
+//                  It also forms D_i = rowsum(dO_i * O_i) (FP32) for its rows.
+//   2. bwd_dkdv  : key-major.  A workgroup owns 64 keys and streams the query
+//                  tiles (Q, dO and z); with lambda already applied it
+//                  accumulates dV = r^T dO, dK^acc = t^T Q and C = r^T z and
+//                  writes dK = BF16(fl32[alpha (dK^acc - C)]).
 // Both passes rebuild P, r and t with identical instructions, so the r and t
 // of the key pass equal those of the query pass bitwise, and lambda is divided
 // once.  gproj_q runs the plain key-major pass; gproj runs the plain
@@ -40,65 +40,74 @@ namespace gpa {
 namespace {
 
 
-// ---------------------------------------------------------------- preprocess
-template <int D>
-__global__ __launch_bounds__(256) void bwd_pre_kernel(const uint16_t* __restrict__ O,
-                                                      const uint16_t* __restrict__ dO,
-                                                      float* __restrict__ Drow, int rows) {
-    constexpr int TPR = D / 8;  // lanes per row, 8 elements each
-    const int gid = blockIdx.x * 256 + threadIdx.x;
-    const int row = gid / TPR;
-    const int part = gid - row * TPR;
-    float acc = 0.f;
-    if (row < rows) {
-        const u32x4 o = *reinterpret_cast<const u32x4*>(O + (size_t)row * D + part * 8);
-        const u32x4 u = *reinterpret_cast<const u32x4*>(dO + (size_t)row * D + part * 8);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            // BF16 x BF16 products are exact in FP32.
-            acc += lo_bf16(u[e]) * lo_bf16(o[e]);
-            acc += hi_bf16(u[e]) * hi_bf16(o[e]);
-        }
-    }
-#pragma unroll
-    for (int off = TPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-    if (row < rows && part == 0) Drow[row] = acc;
-}
-
 // --------------------------------------------------------- query-major pass
-// P, r, t for one key tile of the query-major pass: lane holds keys 4g+i of
-// each 16-key block for its query.  MASK applies causal and tail masks (only
-// diagonal and tail tiles need them).
+// P, r, t for 32 keys (two 16-key blocks) of the query-major pass: lane holds
+// keys 4g+i of each block for its query.  MASK applies the causal and tail
+// masks (only diagonal and tail tiles need them).
 template <bool MASK>
-__device__ __forceinline__ void dq_probs(const f32x4 (&s)[4], const f32x4 (&dp)[4], float c,
-                                         float lse2, float Di, int k0, int g, int qrow, bool qok,
-                                         int N, int causal, bf16x8 (&tf)[2], bf16x8 (&rf)[2]) {
+__device__ __forceinline__ void dq_probs(const f32x4 (&s)[2], const f32x4 (&dp)[2], float c,
+                                         float lse2, float Di, int key0, int g, int qrow,
+                                         bool qok, int N, int causal, bf16x8& tf, bf16x8& rf) {
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             float P = fexp2(fmaf(s[kb][i], c, -lse2));
             if constexpr (MASK) {
-                const int key = k0 + kb * 16 + 4 * g + i;
+                const int key = key0 + kb * 16 + 4 * g + i;
                 const bool ok = qok && key < N && (!causal || key <= qrow);
                 P = ok ? P : 0.f;
             }
-            tf[kb >> 1][(kb & 1) * 4 + i] = to_bf16(P * (dp[kb][i] - Di));
-            rf[kb >> 1][(kb & 1) * 4 + i] = to_bf16(P);
+            tf[kb * 4 + i] = to_bf16(P * (dp[kb][i] - Di));
+            rf[kb * 4 + i] = to_bf16(P);
         }
 }
 
-template <int D, bool GPROJ>
-__global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
+// Stage one 64-row tile of up to three BF16 tensors (global -> registers ->
+// swizzled LDS).  Rows at or beyond N are zero.
+template <int D, int NT>
+struct TileStager {
+    static constexpr int CH = kTile * D / 8 / kThreads;  // 16-byte chunks per thread
+    u32x4 reg[NT][CH];
+
+    __device__ __forceinline__ void fetch(const uint16_t* const (&src)[NT], int row0, int N,
+                                          int tid) {
+        const bool full = row0 + kTile <= N;
+#pragma unroll
+        for (int cI = 0; cI < CH; ++cI) {
+            const int ch = tid + cI * kThreads;
+            const int r = ch / (D / 8);
+            const int cc = (ch - r * (D / 8)) * 8;
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+                reg[t][cI] = full ? *reinterpret_cast<const u32x4*>(src[t] + (size_t)(row0 + r) * D + cc)
+                                  : ld_row16(src[t], row0 + r, N, D, cc);
+        }
+    }
+    __device__ __forceinline__ void store(uint16_t* const (&dst)[NT], int tid) const {
+#pragma unroll
+        for (int cI = 0; cI < CH; ++cI) {
+            const int ch = tid + cI * kThreads;
+            const int r = ch / (D / 8);
+            const int cc = (ch - r * (D / 8)) * 8;
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+                *reinterpret_cast<u32x4*>(dst[t] + tile_off<D>(r, cc)) = reg[t][cI];
+        }
+    }
+};
+
+template <int D, bool GPROJ, bool WRITE_Z>
+__global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 2) void bwd_dq_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
-    const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
-    const float* __restrict__ LSE, const float* __restrict__ Drow, uint16_t* __restrict__ dQ,
-    float* __restrict__ rho_out, float* __restrict__ m_out, float* __restrict__ lam_out,
-    int BH, int N, int causal, float scale) {
-    constexpr int RP = Pitch<D>::row;
-    constexpr int CH = kTile * D / 8 / kThreads;  // 16-byte chunks per thread per tile
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[kTile * RP];  // K row-major
-    __shared__ __attribute__((aligned(16))) uint16_t Vs[kTile * RP];  // V row-major
+    const uint16_t* __restrict__ V, const uint16_t* __restrict__ O,
+    const uint16_t* __restrict__ dO, const float* __restrict__ LSE, float* __restrict__ D_out,
+    uint16_t* __restrict__ dQ, float* __restrict__ rho_out, float* __restrict__ m_out,
+    float* __restrict__ lam_out, uint16_t* __restrict__ Zout, int BH, int N, int causal,
+    float scale) {
+    // Double-buffered K and V tiles (row-major, swizzled).
+    __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kTile * D];
+    __shared__ __attribute__((aligned(16))) uint16_t Vs[2][kTile * D];
 
     const int T = (N + kTile - 1) / kTile;
     int bh, tile;
@@ -118,9 +127,23 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
         qf[kc] = __builtin_bit_cast(bf16x8, ld_row16(Q + hoff, qrow, N, D, kc * 32 + 8 * g));
         uf[kc] = __builtin_bit_cast(bf16x8, ld_row16(dO + hoff, qrow, N, D, kc * 32 + 8 * g));
     }
+    // Algorithm 1's preprocessing, fused: D_i = sum_c fl32(dO_ic O_ic) (BF16 x BF16
+    // products are exact in FP32), from this lane's column slices of the row,
+    // summed over the row's 4 lanes.  The key-major pass reads D back.
+    float dpart = 0.f;
+#pragma unroll
+    for (int kc = 0; kc < D / 32; ++kc) {
+        const u32x4 ow = ld_row16(O + hoff, qrow, N, D, kc * 32 + 8 * g);
+        const u32x4 uw = __builtin_bit_cast(u32x4, uf[kc]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            dpart += lo_bf16(uw[e]) * lo_bf16(ow[e]);
+            dpart += hi_bf16(uw[e]) * hi_bf16(ow[e]);
+        }
+    }
+    const float Di = xor_sum(dpart);
     const float c = scale * kLog2e;
     const float lse2 = LSE[ridx] * kLog2e;
-    const float Di = Drow[ridx];
     const bf16x8 ones = ones_row0(c16);
 
     f32x4 accA[D / 16], accB[GPROJ ? D / 16 : 1];
@@ -133,69 +156,63 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
     const int nkv = causal ? min(T, tile + 1) : T;
     const bool q_tail = tile * kTile + kTile > N;
 
-    u32x4 kreg[CH], vreg[CH];
-    auto fetch = [&](int k0) {
-#pragma unroll
-        for (int cI = 0; cI < CH; ++cI) {
-            const int ch = tid + cI * kThreads;
-            const int r = ch / (D / 8);
-            const int cc = (ch - r * (D / 8)) * 8;
-            kreg[cI] = ld_row16(K + hoff, k0 + r, N, D, cc);
-            vreg[cI] = ld_row16(V + hoff, k0 + r, N, D, cc);
-        }
-    };
-    fetch(0);
+    TileStager<D, 2> st;
+    const uint16_t* const src[2] = {K + hoff, V + hoff};
+    st.fetch(src, 0, N, tid);
+    {
+        uint16_t* const dst[2] = {Ks[0], Vs[0]};
+        st.store(dst, tid);
+    }
+    __syncthreads();
     for (int kt = 0; kt < nkv; ++kt) {
         const int k0 = kt * kTile;
-        __syncthreads();
-#pragma unroll
-        for (int cI = 0; cI < CH; ++cI) {
-            const int ch = tid + cI * kThreads;
-            const int r = ch / (D / 8);
-            const int cc = (ch - r * (D / 8)) * 8;
-            *reinterpret_cast<u32x4*>(Ks + r * RP + cc) = kreg[cI];
-            *reinterpret_cast<u32x4*>(Vs + r * RP + cc) = vreg[cI];
-        }
-        __syncthreads();
-        if (kt + 1 < nkv) fetch(k0 + kTile);
-
-        // S^T = K Q^T and dP^T = V dO^T: lane holds keys 4g+i of each 16-key
-        // block for its own query.
-        f32x4 s[4], dp[4];
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-            s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-            dp[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int kc = 0; kc < D / 32; ++kc) {
-                s[kb] = mfma_16x16x32(ld_b128(Ks + (kb * 16 + c16) * RP + kc * 32 + 8 * g), qf[kc],
-                                      s[kb]);
-                dp[kb] = mfma_16x16x32(ld_b128(Vs + (kb * 16 + c16) * RP + kc * 32 + 8 * g),
-                                       uf[kc], dp[kb]);
-            }
-        }
-        bf16x8 tf[2], rf[2];
+        const int cur = kt & 1;
+        if (kt + 1 < nkv) st.fetch(src, k0 + kTile, N, tid);
+        const uint16_t* Kc = Ks[cur];
+        const uint16_t* Vc = Vs[cur];
         const bool edge = (causal && kt == tile) || q_tail || k0 + kTile > N;
-        if (edge)
-            dq_probs<true>(s, dp, c, lse2, Di, k0, g, qrow, qok, N, causal, tf, rf);
-        else
-            dq_probs<false>(s, dp, c, lse2, Di, k0, g, qrow, qok, N, causal, tf, rf);
 
-        // A^T[d][query] += K^T[d][key] t^T[key][query]  (and B^T with r); the
-        // row sums rho, m come from a constant ones operand.
+        // Two halves of 32 keys.  S^T = K Q^T and dP^T = V dO^T leave each lane
+        // with keys 4g+i of each 16-key block for its own query.
 #pragma unroll
-        for (int kc2 = 0; kc2 < 2; ++kc2) {
+        for (int h = 0; h < 2; ++h) {
+            f32x4 s[2], dp[2];
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                const int kb = 2 * h + b;
+                s[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+                dp[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int kc = 0; kc < D / 32; ++kc) {
+                    s[b] = mfma_16x16x32(ld_b128(Kc + tile_off<D>(kb * 16 + c16, kc * 32 + 8 * g)),
+                                         qf[kc], s[b]);
+                    dp[b] = mfma_16x16x32(ld_b128(Vc + tile_off<D>(kb * 16 + c16, kc * 32 + 8 * g)),
+                                          uf[kc], dp[b]);
+                }
+            }
+            bf16x8 tf, rf;
+            if (edge)
+                dq_probs<true>(s, dp, c, lse2, Di, k0 + 32 * h, g, qrow, qok, N, causal, tf, rf);
+            else
+                dq_probs<false>(s, dp, c, lse2, Di, k0 + 32 * h, g, qrow, qok, N, causal, tf, rf);
+            // A^T[d][query] += K^T[d][key] t^T[key][query] (and B^T with r); the
+            // row sums rho, m come from a constant ones operand.
 #pragma unroll
             for (int mb = 0; mb < D / 16; ++mb) {
-                const bf16x8 ka = ld_tr_operand(Ks, RP, kc2 * 32, mb * 16, c16, g);
-                accA[mb] = mfma_16x16x32(ka, tf[kc2], accA[mb]);
-                if (GPROJ) accB[mb] = mfma_16x16x32(ka, rf[kc2], accB[mb]);
+                const bf16x8 ka = ld_tr_operand<D>(Kc, h * 32, mb * 16, c16, g);
+                accA[mb] = mfma_16x16x32(ka, tf, accA[mb]);
+                if (GPROJ) accB[mb] = mfma_16x16x32(ka, rf, accB[mb]);
             }
             if (GPROJ) {
-                accR = mfma_16x16x32(ones, tf[kc2], accR);
-                accM = mfma_16x16x32(ones, rf[kc2], accM);
+                accR = mfma_16x16x32(ones, tf, accR);
+                accM = mfma_16x16x32(ones, rf, accM);
             }
         }
+        if (kt + 1 < nkv) {
+            uint16_t* const dst[2] = {Ks[cur ^ 1], Vs[cur ^ 1]};
+            st.store(dst, tid);
+        }
+        __syncthreads();
     }
 
     // rho and m of this lane's query sit in accumulator row 0 (lanes g == 0).
@@ -223,7 +240,19 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
             }
             st_bf16x4(drow + mb * 16 + 4 * g, v[0], v[1], v[2], v[3]);
         }
+        if (WRITE_Z) {
+            // z = BF16(fl32(lambda q)) for the key correction: the lane holds
+            // d = kc*32 + 8g .. +7 of its query row.
+#pragma unroll
+            for (int kc = 0; kc < D / 32; ++kc) {
+                bf16x8 z;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) z[e] = to_bf16(lam * bf16_to_f32(qf[kc][e]));
+                *reinterpret_cast<bf16x8*>(Zout + hoff + (size_t)qrow * D + kc * 32 + 8 * g) = z;
+            }
+        }
         if (g == 0) {
+            D_out[ridx] = Di;
             rho_out[ridx] = rho;
             m_out[ridx] = msum;
             lam_out[ridx] = lam;
@@ -232,42 +261,39 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
 }
 
 // ----------------------------------------------------------- key-major pass
-// P, r, t for one query tile of the key-major pass: lane holds queries 4g+i of
-// each 16-query block for its key.
+// P, r, t for 32 queries (two 16-query blocks) of the key-major pass: lane
+// holds queries 4g+i of each block for its key.
 template <bool MASK>
-__device__ __forceinline__ void dkdv_probs(const f32x4 (&s)[4], const f32x4 (&dp)[4],
-                                           const f32x4 (&l2)[4], const f32x4 (&dd)[4], float c,
-                                           int q0, int g, int krow, int N, int causal,
-                                           bf16x8 (&tf)[2], bf16x8 (&rf)[2]) {
+__device__ __forceinline__ void dkdv_probs(const f32x4 (&s)[2], const f32x4 (&dp)[2],
+                                           const f32x4 (&l2)[2], const f32x4 (&dd)[2], float c,
+                                           int qb0, int g, int krow, int N, int causal,
+                                           bf16x8& tf, bf16x8& rf) {
 #pragma unroll
-    for (int mq = 0; mq < 4; ++mq)
+    for (int b = 0; b < 2; ++b)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            float P = fexp2(fmaf(s[mq][i], c, -l2[mq][i]));
+            float P = fexp2(fmaf(s[b][i], c, -l2[b][i]));
             if constexpr (MASK) {
-                const int query = q0 + mq * 16 + 4 * g + i;
+                const int query = qb0 + b * 16 + 4 * g + i;
                 const bool ok = krow < N && query < N && (!causal || krow <= query);
                 P = ok ? P : 0.f;
             }
-            tf[mq >> 1][(mq & 1) * 4 + i] = to_bf16(P * (dp[mq][i] - dd[mq][i]));
-            rf[mq >> 1][(mq & 1) * 4 + i] = to_bf16(P);
+            tf[b * 4 + i] = to_bf16(P * (dp[b][i] - dd[b][i]));
+            rf[b * 4 + i] = to_bf16(P);
         }
 }
 
 template <int D, bool GPROJ>
-__global__ __launch_bounds__(kThreads, D == 64 ? 2 : 1) void bwd_dkdv_kernel(
+__global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dkdv_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
     const float* __restrict__ LSE, const float* __restrict__ Drow,
-    const float* __restrict__ lam, uint16_t* __restrict__ dK, uint16_t* __restrict__ dV,
+    const uint16_t* __restrict__ Z, uint16_t* __restrict__ dK, uint16_t* __restrict__ dV,
     int BH, int N, int causal, float scale) {
-    constexpr int RP = Pitch<D>::row;
-    constexpr int CH = kTile * D / 8 / kThreads;
-    __shared__ __attribute__((aligned(16))) uint16_t Qs[kTile * RP];   // Q row-major
-    __shared__ __attribute__((aligned(16))) uint16_t Us[kTile * RP];   // dO row-major
-    __shared__ __attribute__((aligned(16))) uint16_t Zs[GPROJ ? kTile * RP : 8];  // BF16(lambda q)
-    __shared__ __attribute__((aligned(16))) float lse2s[kTile];
-    __shared__ __attribute__((aligned(16))) float Ds[kTile];
+    constexpr int NT = GPROJ ? 3 : 2;  // staged tensors: Q, dO (and Z = BF16(lambda Q))
+    __shared__ __attribute__((aligned(16))) uint16_t Ts[2][NT][kTile * D];
+    __shared__ __attribute__((aligned(16))) float lse2s[2][kTile];
+    __shared__ __attribute__((aligned(16))) float Ds[2][kTile];
 
     const int T = (N + kTile - 1) / kTile;
     int bh, tile;
@@ -301,95 +327,82 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 2 : 1) void bwd_dkdv_kernel(
     const int qt0 = causal ? tile : 0;
     const bool k_tail = tile * kTile + kTile > N;
 
-    u32x4 qreg[CH], ureg[CH];
-    float lreg[CH];
+    TileStager<D, NT> st;
+    const uint16_t* src[NT];
+    src[0] = Q + hoff;
+    src[1] = dO + hoff;
+    if (GPROJ) src[NT - 1] = Z + hoff;
     float lse_reg = 0.f, d_reg = 0.f;
-    auto fetch = [&](int q0) {
-#pragma unroll
-        for (int cI = 0; cI < CH; ++cI) {
-            const int ch = tid + cI * kThreads;
-            const int r = ch / (D / 8);
-            const int cc = (ch - r * (D / 8)) * 8;
-            qreg[cI] = ld_row16(Q + hoff, q0 + r, N, D, cc);
-            ureg[cI] = ld_row16(dO + hoff, q0 + r, N, D, cc);
-            if (GPROJ) lreg[cI] = lam[soff + min(q0 + r, N - 1)];
-        }
+    auto fetch_stats = [&](int q0) {
         if (tid < kTile) {
             const int row = min(q0 + tid, N - 1);
             lse_reg = LSE[soff + row];
             d_reg = Drow[soff + row];
         }
     };
-    fetch(qt0 * kTile);
+    auto store = [&](int buf) {
+        uint16_t* dst[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) dst[t] = Ts[buf][t];
+        st.store(dst, tid);
+        if (tid < kTile) {
+            lse2s[buf][tid] = lse_reg * kLog2e;
+            Ds[buf][tid] = d_reg;
+        }
+    };
+    st.fetch(src, qt0 * kTile, N, tid);
+    fetch_stats(qt0 * kTile);
+    store(0);
+    __syncthreads();
     for (int qt = qt0; qt < T; ++qt) {
         const int q0 = qt * kTile;
-        __syncthreads();
-#pragma unroll
-        for (int cI = 0; cI < CH; ++cI) {
-            const int ch = tid + cI * kThreads;
-            const int r = ch / (D / 8);
-            const int cc = (ch - r * (D / 8)) * 8;
-            const u32x4 qw = qreg[cI];
-            *reinterpret_cast<u32x4*>(Qs + r * RP + cc) = qw;
-            *reinterpret_cast<u32x4*>(Us + r * RP + cc) = ureg[cI];
-            if (GPROJ) {
-                // z = BF16(fl32(lambda q))
-                u32x4 zw;
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    zw[e] = (uint32_t)bf16_bits(lreg[cI] * lo_bf16(qw[e])) |
-                            ((uint32_t)bf16_bits(lreg[cI] * hi_bf16(qw[e])) << 16);
-                *reinterpret_cast<u32x4*>(Zs + r * RP + cc) = zw;
-            }
+        const int cur = (qt - qt0) & 1;
+        if (qt + 1 < T) {
+            st.fetch(src, q0 + kTile, N, tid);
+            fetch_stats(q0 + kTile);
         }
-        if (tid < kTile) {
-            lse2s[tid] = lse_reg * kLog2e;
-            Ds[tid] = d_reg;
-        }
-        __syncthreads();
-        if (qt + 1 < T) fetch(q0 + kTile);
-
-        // S = Q K^T and dP = dO V^T: lane holds queries 4g+i of each 16-query
-        // block for its own key.
-        f32x4 s[4], dp[4];
-#pragma unroll
-        for (int mq = 0; mq < 4; ++mq) {
-            s[mq] = f32x4{0.f, 0.f, 0.f, 0.f};
-            dp[mq] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int kc = 0; kc < D / 32; ++kc) {
-                s[mq] = mfma_16x16x32(ld_b128(Qs + (mq * 16 + c16) * RP + kc * 32 + 8 * g), kf[kc],
-                                      s[mq]);
-                dp[mq] = mfma_16x16x32(ld_b128(Us + (mq * 16 + c16) * RP + kc * 32 + 8 * g),
-                                       vf[kc], dp[mq]);
-            }
-        }
-        f32x4 l2[4], dd[4];
-#pragma unroll
-        for (int mq = 0; mq < 4; ++mq) {
-            l2[mq] = *reinterpret_cast<const f32x4*>(lse2s + mq * 16 + 4 * g);
-            dd[mq] = *reinterpret_cast<const f32x4*>(Ds + mq * 16 + 4 * g);
-        }
-        bf16x8 tf[2], rf[2];
+        const uint16_t* Qc = Ts[cur][0];
+        const uint16_t* Uc = Ts[cur][1];
+        const uint16_t* Zc = Ts[cur][NT - 1];
         const bool edge = (causal && qt == tile) || k_tail || q0 + kTile > N;
-        if (edge)
-            dkdv_probs<true>(s, dp, l2, dd, c, q0, g, krow, N, causal, tf, rf);
-        else
-            dkdv_probs<false>(s, dp, l2, dd, c, q0, g, krow, N, causal, tf, rf);
 
-        // dV^T[dv][key] += dO^T r ; dK^T += Q^T t ; C^T += Z^T r.
+        // Two halves of 32 queries.  S = Q K^T and dP = dO V^T leave each lane
+        // with queries 4g+i of each 16-query block for its own key.
 #pragma unroll
-        for (int mb = 0; mb < D / 16; ++mb)
+        for (int h = 0; h < 2; ++h) {
+            f32x4 s[2], dp[2], l2[2], dd[2];
 #pragma unroll
-            for (int kc2 = 0; kc2 < 2; ++kc2) {
-                accV[mb] = mfma_16x16x32(ld_tr_operand(Us, RP, kc2 * 32, mb * 16, c16, g), rf[kc2],
-                                         accV[mb]);
-                accK[mb] = mfma_16x16x32(ld_tr_operand(Qs, RP, kc2 * 32, mb * 16, c16, g), tf[kc2],
-                                         accK[mb]);
-                if (GPROJ)
-                    accC[mb] = mfma_16x16x32(ld_tr_operand(Zs, RP, kc2 * 32, mb * 16, c16, g),
-                                             rf[kc2], accC[mb]);
+            for (int b = 0; b < 2; ++b) {
+                const int mq = 2 * h + b;
+                s[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+                dp[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int kc = 0; kc < D / 32; ++kc) {
+                    s[b] = mfma_16x16x32(ld_b128(Qc + tile_off<D>(mq * 16 + c16, kc * 32 + 8 * g)),
+                                         kf[kc], s[b]);
+                    dp[b] = mfma_16x16x32(ld_b128(Uc + tile_off<D>(mq * 16 + c16, kc * 32 + 8 * g)),
+                                          vf[kc], dp[b]);
+                }
+                l2[b] = *reinterpret_cast<const f32x4*>(&lse2s[cur][mq * 16 + 4 * g]);
+                dd[b] = *reinterpret_cast<const f32x4*>(&Ds[cur][mq * 16 + 4 * g]);
             }
+            bf16x8 tf, rf;
+            if (edge)
+                dkdv_probs<true>(s, dp, l2, dd, c, q0 + 32 * h, g, krow, N, causal, tf, rf);
+            else
+                dkdv_probs<false>(s, dp, l2, dd, c, q0 + 32 * h, g, krow, N, causal, tf, rf);
+            // dV^T[dv][key] += dO^T r ; dK^T += Q^T t ; C^T += Z^T r.
+#pragma unroll
+            for (int mb = 0; mb < D / 16; ++mb) {
+                accV[mb] = mfma_16x16x32(ld_tr_operand<D>(Uc, h * 32, mb * 16, c16, g), rf, accV[mb]);
+                accK[mb] = mfma_16x16x32(ld_tr_operand<D>(Qc, h * 32, mb * 16, c16, g), tf, accK[mb]);
+                if (GPROJ)
+                    accC[mb] = mfma_16x16x32(ld_tr_operand<D>(Zc, h * 32, mb * 16, c16, g), rf,
+                                             accC[mb]);
+            }
+        }
+        if (qt + 1 < T) store(cur ^ 1);
+        __syncthreads();
     }
 
     if (kok) {
@@ -416,32 +429,23 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 2 : 1) void bwd_dkdv_kernel(
 
 }  // namespace
 
-hipError_t launch_bwd_pre(const uint16_t* O, const uint16_t* dO, float* Drow, const Shape& s,
-                          hipStream_t st) {
-    const long rows = (long)s.BH * s.N;
-    const int tpr = s.d / 8;
-    const unsigned blocks = (unsigned)((rows * tpr + 255) / 256);
-    if (s.d == 64)
-        bwd_pre_kernel<64><<<blocks, 256, 0, st>>>(O, dO, Drow, (int)rows);
-    else
-        bwd_pre_kernel<128><<<blocks, 256, 0, st>>>(O, dO, Drow, (int)rows);
-    return hipGetLastError();
-}
-
 hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                         const uint16_t* dO, const float* LSE, const float* Drow, uint16_t* dQ,
-                         float* rho, float* msum, float* lambda, int mode, const Shape& s,
-                         hipStream_t st) {
+                         const uint16_t* O, const uint16_t* dO, const float* LSE, float* Drow,
+                         uint16_t* dQ, float* rho, float* msum, float* lambda, uint16_t* Z,
+                         int mode, const Shape& s, hipStream_t st) {
     const int T = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
-    const bool gp = mode != 0;
-#define GPA_DQ(DD, GP)                                                                       \
-    bwd_dq_kernel<DD, GP><<<grid, block, 0, st>>>(Q, K, V, dO, LSE, Drow, dQ, rho, msum, lambda, \
-                                                  s.BH, s.N, s.causal, s.scale)
+#define GPA_DQ(DD, GP, WZ)                                                                  \
+    bwd_dq_kernel<DD, GP, WZ><<<grid, block, 0, st>>>(Q, K, V, O, dO, LSE, Drow, dQ, rho, msum, \
+                                                      lambda, Z, s.BH, s.N, s.causal, s.scale)
     if (s.d == 64) {
-        if (gp) GPA_DQ(64, true); else GPA_DQ(64, false);
+        if (mode == 2) GPA_DQ(64, true, true);
+        else if (mode == 1) GPA_DQ(64, true, false);
+        else GPA_DQ(64, false, false);
     } else {
-        if (gp) GPA_DQ(128, true); else GPA_DQ(128, false);
+        if (mode == 2) GPA_DQ(128, true, true);
+        else if (mode == 1) GPA_DQ(128, true, false);
+        else GPA_DQ(128, false, false);
     }
 #undef GPA_DQ
     return hipGetLastError();
@@ -449,13 +453,13 @@ hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V
 
 hipError_t launch_bwd_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                            const uint16_t* dO, const float* LSE, const float* Drow,
-                           const float* lambda, uint16_t* dK, uint16_t* dV, int mode,
+                           const uint16_t* Z, uint16_t* dK, uint16_t* dV, int mode,
                            const Shape& s, hipStream_t st) {
     const int T = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
     const bool gp = mode == 2;
-#define GPA_DKDV(DD, GP)                                                                  \
-    bwd_dkdv_kernel<DD, GP><<<grid, block, 0, st>>>(Q, K, V, dO, LSE, Drow, lambda, dK, dV, \
+#define GPA_DKDV(DD, GP)                                                             \
+    bwd_dkdv_kernel<DD, GP><<<grid, block, 0, st>>>(Q, K, V, dO, LSE, Drow, Z, dK, dV, \
                                                     s.BH, s.N, s.causal, s.scale)
     if (s.d == 64) {
         if (gp) GPA_DKDV(64, true); else GPA_DKDV(64, false);

@@ -20,16 +20,6 @@ constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kTile = 64;  // rows per workgroup tile and per streamed tile
 
-// LDS row pitches (in 16-bit elements).  Row-major tiles are read 16 bytes per
-// lane by 16 lanes on different rows: a pitch of d+8 elements (d*2+16 bytes)
-// puts consecutive rows 4 banks apart.  Transposed tiles are read 8 bytes per
-// lane on 16 different rows: a pitch of 64+4 elements (136 bytes) puts them 2
-// banks apart.
-template <int D> struct Pitch {
-    static constexpr int row = D + 8;
-    static constexpr int tr = kTile + 4;
-};
-
 __device__ __forceinline__ f32x4 mfma_16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
@@ -49,18 +39,35 @@ __device__ __forceinline__ bf16x8 ld_b64x2(const uint16_t* p0, const uint16_t* p
 typedef __bf16 bf16v4_t __attribute__((__vector_size__(8)));
 typedef __attribute__((address_space(3))) bf16v4_t lds_bf16v4_t;
 
+// LDS tiles hold 64 rows x D BF16 values, row-major without padding, with the
+// 16-byte chunks of each row permuted: chunk c of row r lives at chunk
+// c ^ swz(r), swz(r) = ((r & 3) << 1) | ((r >> 2) & 1).  Two read patterns hit
+// these tiles: 16-byte reads of one chunk from 8 consecutive rows (rows
+// r..r+7 land on 8 distinct chunk slots) and transpose reads of 32 bytes from
+// 4 consecutive rows (rows 4g..4g+3 land on disjoint chunk pairs); both are
+// free of bank conflicts, and so are the 16-byte staging writes of whole rows.
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+
+// Element offset of (row r, column col) in a swizzled tile; col % 4 == 0.
+template <int D>
+__device__ __forceinline__ int tile_off(int r, int col) {
+    return r * D + (((col >> 3) ^ swz(r)) << 3) + (col & 7);
+}
+
 // Transposed MFMA operand read straight from a row-major LDS tile X[k][n]
-// (pitch P elements) with the gfx950 LDS transpose load ds_read_b64_tr_b16.
-// Within each 16-lane group, that instruction hands lane j element j of the
-// 4 x 16 block formed by the 8-byte reads of lanes 4r+q (row r, columns
-// 4q..4q+3).  Addressing rows k0+4g+r and columns n0+4q therefore gives lane
-// (c16, g) the values X[k0 + 4g + r][n0 + c16], r = 0..3; a second read 16 rows
-// further down fills elements 4..7.  This is the k-layout {4g+r, 16+4g+r} that
-// the 16x16 accumulator of the preceding product leaves in each lane.
-__device__ __forceinline__ bf16x8 ld_tr_operand(const uint16_t* X, int P, int k0, int n0,
-                                                int c16, int g) {
-    const uint16_t* p0 = X + (k0 + 4 * g + (c16 >> 2)) * P + n0 + 4 * (c16 & 3);
-    const uint16_t* p1 = p0 + 16 * P;
+// with the gfx950 LDS transpose load ds_read_b64_tr_b16.  Within each 16-lane
+// group, that instruction hands lane j element j of the 4 x 16 block formed by
+// the 8-byte reads of lanes 4r+q (row r, columns 4q..4q+3).  Addressing rows
+// k0+4g+r and columns n0+4q therefore gives lane (c16, g) the values
+// X[k0 + 4g + r][n0 + c16], r = 0..3; a second read 16 rows further down fills
+// elements 4..7.  This is the k-layout {4g+r, 16+4g+r} that the 16x16
+// accumulator of the preceding product leaves in each lane.
+template <int D>
+__device__ __forceinline__ bf16x8 ld_tr_operand(const uint16_t* X, int k0, int n0, int c16,
+                                                int g) {
+    const int row = k0 + 4 * g + (c16 >> 2);
+    const uint16_t* p0 = X + tile_off<D>(row, n0 + 4 * (c16 & 3));
+    const uint16_t* p1 = p0 + 16 * D;  // row + 16 has the same swizzle
     const bf16x4 a =
         __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16v4_t*)p0));
     const bf16x4 b =
@@ -123,22 +130,36 @@ __device__ __forceinline__ float xor_sum(float v) {
 }
 
 // Workgroup -> (batch*head, tile).  Workgroups are dispatched round-robin over
-// the 8 XCDs (each with its own L2), so when the grid divides evenly, XCD x is
-// given a contiguous range of (head, tile) pairs: the tiles of one head share
-// that XCD's L2.  Within a head, tiles go out in the order given by
-// heavy_first_desc (descending tile index for the query-major causal kernels,
-// whose last tiles have the most work; ascending for the key-major ones).
-__device__ __forceinline__ void map_block(int bid, int BH, int T, bool heavy_first_desc,
-                                          int* bh, int* tile) {
-    const int nwg = BH * T;
-    int linear = bid;
-    if ((nwg & 7) == 0) {
-        const int per = nwg >> 3;
-        linear = (bid & 7) * per + (bid >> 3);
+// the 8 XCDs (each with its own L2), and within an XCD to whichever slots free
+// up first.  When B*H is a multiple of 8, XCD x owns heads [x*BH/8, (x+1)*BH/8)
+// so one head's tiles share an L2.  Within that set the order is rank-major:
+// every head's heaviest tile, then every head's next heaviest, ... , which makes
+// the hardware's in-order dispatch a longest-first greedy schedule for any
+// number of resident workgroups.  heavy_high selects which end is heavy: the
+// query-major causal kernels' last tiles do the most work, the key-major
+// kernels' first tiles do.
+__device__ __forceinline__ void map_block(int bid, int BH, int T, bool heavy_high, int* bh,
+                                          int* tile) {
+    int heads = BH, base = 0, li = bid;
+    if ((BH & 7) == 0) {
+        heads = BH >> 3;
+        base = (bid & 7) * heads;
+        li = bid >> 3;
     }
-    *bh = linear / T;
-    const int t = linear - (*bh) * T;
-    *tile = heavy_first_desc ? (T - 1 - t) : t;
+    const int rank = li / heads;
+    *bh = base + (li - rank * heads);
+    *tile = heavy_high ? (T - 1 - rank) : rank;
 }
+
+// Target waves per SIMD of each MFMA kernel (build-time tuning constants).
+#ifndef GPA_FWD_OCC
+#define GPA_FWD_OCC 2
+#endif
+#ifndef GPA_DQ_OCC64
+#define GPA_DQ_OCC64 3
+#endif
+#ifndef GPA_DKDV_OCC64
+#define GPA_DKDV_OCC64 2
+#endif
 
 }  // namespace gpa

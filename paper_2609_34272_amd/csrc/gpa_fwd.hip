@@ -18,14 +18,13 @@ namespace gpa {
 namespace {
 
 template <int D>
-__global__ __launch_bounds__(kThreads, 2) void fwd_sbs_kernel(
+__global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, uint16_t* __restrict__ O, float* __restrict__ LSE,
     int BH, int N, int causal, float scale) {
-    constexpr int RP = Pitch<D>::row;
     constexpr int CH = kTile * D / 8 / kThreads;
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[kTile * RP];
-    __shared__ __attribute__((aligned(16))) uint16_t Vs[kTile * RP];
+    __shared__ __attribute__((aligned(16))) uint16_t Ks[kTile * D];
+    __shared__ __attribute__((aligned(16))) uint16_t Vs[kTile * D];
 
     const int T = (N + kTile - 1) / kTile;
     int bh, tile;
@@ -73,8 +72,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_sbs_kernel(
             const int ch = tid + cI * kThreads;
             const int r = ch / (D / 8);
             const int cc = (ch - r * (D / 8)) * 8;
-            *reinterpret_cast<u32x4*>(Ks + r * RP + cc) = kreg[cI];
-            *reinterpret_cast<u32x4*>(Vs + r * RP + cc) = vreg[cI];
+            *reinterpret_cast<u32x4*>(Ks + tile_off<D>(r, cc)) = kreg[cI];
+            *reinterpret_cast<u32x4*>(Vs + tile_off<D>(r, cc)) = vreg[cI];
         }
         __syncthreads();
         if (kt + 1 < nkv) fetch(k0 + kTile);
@@ -86,7 +85,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_sbs_kernel(
             s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int kc = 0; kc < D / 32; ++kc)
-                s[kb] = mfma_16x16x32(ld_b128(Ks + (kb * 16 + c16) * RP + kc * 32 + 8 * g), qf[kc],
+                s[kb] = mfma_16x16x32(ld_b128(Ks + tile_off<D>(kb * 16 + c16, kc * 32 + 8 * g)), qf[kc],
                                       s[kb]);
         }
         // Only the diagonal tile and the key tail need masks (uniform branch).
@@ -130,7 +129,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_sbs_kernel(
         for (int mb = 0; mb < D / 16; ++mb)
 #pragma unroll
             for (int kc2 = 0; kc2 < 2; ++kc2)
-                acc[mb] = mfma_16x16x32(ld_tr_operand(Vs, RP, kc2 * 32, mb * 16, c16, g), pf[kc2],
+                acc[mb] = mfma_16x16x32(ld_tr_operand<D>(Vs, kc2 * 32, mb * 16, c16, g), pf[kc2],
                                         acc[mb]);
     }
 

@@ -18,33 +18,30 @@ struct Shape {
 // Kernel ids for timing (gpa_profile_*).
 enum KernelId {
     kKFwd = 0,
-    kKBwdPre = 1,
-    kKBwdDq = 2,
-    kKBwdDkdv = 3,
-    kKF32Fwd = 4,
-    kKF32Pre = 5,
-    kKF32Dq = 6,
-    kKF32Dkdv = 7,
-    kNumKernels = 8
+    kKBwdDq = 1,
+    kKBwdDkdv = 2,
+    kKF32Fwd = 3,
+    kKF32Pre = 4,
+    kKF32Dq = 5,
+    kKF32Dkdv = 6,
+    kNumKernels = 7
 };
 
 hipError_t launch_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, uint16_t* O,
                       float* LSE, const Shape& s, hipStream_t st);
 
-hipError_t launch_bwd_pre(const uint16_t* O, const uint16_t* dO, float* Drow, const Shape& s,
-                          hipStream_t st);
-
-// Query-major pass: t K (and r K, rho, m in the gproj modes), writes dQ and,
-// in the gproj modes, rho, m, lambda.  In plain mode rho, m, lambda are zeroed.
+// Query-major pass: writes D = rowsum(dO * O) and dQ; in the gproj modes also
+// rho, m, lambda (zero in plain mode); in gproj mode also Z = BF16(lambda Q)
+// ([BH, N, d], BF16).
 hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                         const uint16_t* dO, const float* LSE, const float* Drow, uint16_t* dQ,
-                         float* rho, float* msum, float* lambda, int mode, const Shape& s,
-                         hipStream_t st);
+                         const uint16_t* O, const uint16_t* dO, const float* LSE, float* Drow,
+                         uint16_t* dQ, float* rho, float* msum, float* lambda, uint16_t* Z,
+                         int mode, const Shape& s, hipStream_t st);
 
-// Key-major pass: dV = r^T dO, dK = t^T Q (minus r^T BF16(lambda Q) in gproj mode).
+// Key-major pass: dV = r^T dO, dK = t^T Q (minus r^T Z in gproj mode).
 hipError_t launch_bwd_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                            const uint16_t* dO, const float* LSE, const float* Drow,
-                           const float* lambda, uint16_t* dK, uint16_t* dV, int mode,
+                           const uint16_t* Z, uint16_t* dK, uint16_t* dV, int mode,
                            const Shape& s, hipStream_t st);
 
 // FP32 baseline.
