@@ -11,18 +11,22 @@
 //                  key tiles, so A = tK, B = rK, rho and m stay in registers; at
 //                  the end it forms lambda = rho/m once and writes
 //                  dQ = BF16(fl32[alpha (A - lambda B)]) and lambda.
-//                  In gproj mode it also writes z = BF16(lambda q), once per row.
-//                  It also forms D_i = rowsum(dO_i * O_i) (FP32) for its rows.
+//                  It also forms D_i = rowsum(dO_i * O_i) (FP32) for its rows,
+//                  and in gproj mode writes z = BF16(lambda q), once per row.
 //   2. bwd_dkdv  : key-major.  A workgroup owns 64 keys and streams the query
-//                  tiles (Q, dO and z); with lambda already applied it
-//                  accumulates dV = r^T dO, dK^acc = t^T Q and C = r^T z and
-//                  writes dK = BF16(fl32[alpha (dK^acc - C)]).
+//                  tiles (Q, dO and z); it accumulates dV = r^T dO,
+//                  dK^acc = t^T Q and C = r^T z and writes
+//                  dK = BF16(fl32[alpha (dK^acc - C)]).
 // Both passes rebuild P, r and t with identical instructions, so the r and t
 // of the key pass equal those of the query pass bitwise, and lambda is divided
-// once.  gproj_q runs the plain key-major pass; gproj runs the plain
-// query-major pass plus the correction.  FP32 accumulators, BF16 operands and
-// the cast points are those of the paper; only where lambda becomes available
-// differs.
+// once.  gproj_q runs the GProj query pass and the plain key pass; gproj runs
+// both GProj passes.  FP32 accumulators, BF16 operands and the cast points are
+// those of the paper; only where lambda becomes available differs.
+//
+// Work split inside a workgroup (4 waves).  Each wave owns 32 of the
+// workgroup's 64 rows (two 16-row MFMA blocks that share every LDS operand
+// fragment) and half of each streamed tile; the two waves that own the same
+// rows add their partial accumulators through LDS at the end.
 //
 // MFMA layouts (v_mfma_f32_16x16x32_bf16, wave64): an A operand holds one row
 // per lane (row = lane & 15) and 8 values along k; a B operand holds one column
@@ -39,15 +43,40 @@
 namespace gpa {
 namespace {
 
+// Pairwise reduction of per-lane FP32 partials between waves w and w + 2:
+// waves 2, 3 park their values in LDS (lane-contiguous, conflict-free), waves
+// 0, 1 add them.  `scratch` holds CAP floats; the values go through it in
+// rounds of CAP / 128 per lane.  The caller has synchronised the workgroup so
+// the buffer is free; on return it is free again only after a barrier.
+template <int NV, int CAP>
+__device__ __forceinline__ void pair_reduce(float (&v)[NV], float* scratch, int wave, int lane) {
+    constexpr int PER = CAP / 128;
+    static_assert(PER >= 1, "scratch too small");
+#pragma unroll
+    for (int j0 = 0; j0 < NV; j0 += PER) {
+        if (j0) __syncthreads();
+        if (wave >= 2) {
+            float* p = scratch + (wave - 2) * 64 * PER + lane;
+#pragma unroll
+            for (int j = j0; j < (j0 + PER < NV ? j0 + PER : NV); ++j) p[(j - j0) * 64] = v[j];
+        }
+        __syncthreads();
+        if (wave < 2) {
+            const float* p = scratch + wave * 64 * PER + lane;
+#pragma unroll
+            for (int j = j0; j < (j0 + PER < NV ? j0 + PER : NV); ++j) v[j] += p[(j - j0) * 64];
+        }
+    }
+}
 
 // --------------------------------------------------------- query-major pass
-// P, r, t for 32 keys (two 16-key blocks) of the query-major pass: lane holds
-// keys 4g+i of each block for its query.  MASK applies the causal and tail
-// masks (only diagonal and tail tiles need them).
+// P, r, t of one 32-key x 16-query block pair: s[kb], dp[kb] hold keys
+// 4g+i of key block kb for this lane's query.  MASK applies the causal and
+// tail masks (only diagonal and tail tiles need them).
 template <bool MASK>
 __device__ __forceinline__ void dq_probs(const f32x4 (&s)[2], const f32x4 (&dp)[2], float c,
-                                         float lse2, float Di, int key0, int g, int qrow,
-                                         bool qok, int N, int causal, bf16x8& tf, bf16x8& rf) {
+                                         float lse2, float Di, int key0, int g, int qrow, int N,
+                                         int causal, bf16x8& tf, bf16x8& rf) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -55,7 +84,7 @@ __device__ __forceinline__ void dq_probs(const f32x4 (&s)[2], const f32x4 (&dp)[
             float P = fexp2(fmaf(s[kb][i], c, -lse2));
             if constexpr (MASK) {
                 const int key = key0 + kb * 16 + 4 * g + i;
-                const bool ok = qok && key < N && (!causal || key <= qrow);
+                const bool ok = qrow < N && key < N && (!causal || key <= qrow);
                 P = ok ? P : 0.f;
             }
             tf[kb * 4 + i] = to_bf16(P * (dp[kb][i] - Di));
@@ -63,224 +92,253 @@ __device__ __forceinline__ void dq_probs(const f32x4 (&s)[2], const f32x4 (&dp)[
         }
 }
 
-// Stage one 64-row tile of up to three BF16 tensors (global -> registers ->
-// swizzled LDS).  Rows at or beyond N are zero.
-template <int D, int NT>
-struct TileStager {
-    static constexpr int CH = kTile * D / 8 / kThreads;  // 16-byte chunks per thread
-    u32x4 reg[NT][CH];
-
-    __device__ __forceinline__ void fetch(const uint16_t* const (&src)[NT], int row0, int N,
-                                          int tid) {
-        const bool full = row0 + kTile <= N;
-#pragma unroll
-        for (int cI = 0; cI < CH; ++cI) {
-            const int ch = tid + cI * kThreads;
-            const int r = ch / (D / 8);
-            const int cc = (ch - r * (D / 8)) * 8;
-#pragma unroll
-            for (int t = 0; t < NT; ++t)
-                reg[t][cI] = full ? *reinterpret_cast<const u32x4*>(src[t] + (size_t)(row0 + r) * D + cc)
-                                  : ld_row16(src[t], row0 + r, N, D, cc);
-        }
-    }
-    __device__ __forceinline__ void store(uint16_t* const (&dst)[NT], int tid) const {
-#pragma unroll
-        for (int cI = 0; cI < CH; ++cI) {
-            const int ch = tid + cI * kThreads;
-            const int r = ch / (D / 8);
-            const int cc = (ch - r * (D / 8)) * 8;
-#pragma unroll
-            for (int t = 0; t < NT; ++t)
-                *reinterpret_cast<u32x4*>(dst[t] + tile_off<D>(r, cc)) = reg[t][cI];
-        }
-    }
-};
-
 template <int D, bool GPROJ, bool WRITE_Z>
-__global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 2) void bwd_dq_kernel(
+__global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, const uint16_t* __restrict__ O,
     const uint16_t* __restrict__ dO, const float* __restrict__ LSE, float* __restrict__ D_out,
     uint16_t* __restrict__ dQ, float* __restrict__ rho_out, float* __restrict__ m_out,
     float* __restrict__ lam_out, uint16_t* __restrict__ Zout, int BH, int N, int causal,
     float scale) {
-    // Double-buffered K and V tiles (row-major, swizzled).
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kTile * D];
-    __shared__ __attribute__((aligned(16))) uint16_t Vs[2][kTile * D];
+    constexpr int MB = D / 16;  // 16-column blocks of d
+    constexpr int KC = D / 32;  // 32-wide k chunks of d
+    constexpr int PER_NB = 2 * MB * 4 + 2;  // partial A, B (interleaved) and rho, m
+    // Double-buffered K and V tiles (row-major, swizzled); reused at the end
+    // for the pairwise reduction.
+    // Two separate LDS objects per buffer so the compiler can tell the tile
+    // being read from the one the DMA is filling.
+    __shared__ __attribute__((aligned(16))) uint16_t KV0[2][kTile * D];  // [K, V], buffer 0
+    __shared__ __attribute__((aligned(16))) uint16_t KV1[2][kTile * D];  // [K, V], buffer 1
 
     const int T = (N + kTile - 1) / kTile;
     int bh, tile;
     map_block(blockIdx.x, BH, T, causal != 0, &bh, &tile);
     const size_t hoff = (size_t)bh * N * D;
+    const size_t soff = (size_t)bh * N;
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
-    const int qrow = tile * kTile + wave * 16 + c16;
-    const bool qok = qrow < N;
-    const int qcl = qok ? qrow : N - 1;
-    const size_t ridx = (size_t)bh * N + qcl;
+    const int qh = wave & 1;   // which 32 of the workgroup's 64 queries
+    const int kh = wave >> 1;  // which 32 of each 64-key tile
+    const int q0w = tile * kTile + 32 * qh;
 
-    bf16x8 qf[D / 32], uf[D / 32];
+    // Q^T and dO^T as B operands: column = this lane's query of block nb, k = d.
+    bf16x8 qf[2][KC], uf[2][KC];
+    float lse2[2], Di[2];
 #pragma unroll
-    for (int kc = 0; kc < D / 32; ++kc) {
-        qf[kc] = __builtin_bit_cast(bf16x8, ld_row16(Q + hoff, qrow, N, D, kc * 32 + 8 * g));
-        uf[kc] = __builtin_bit_cast(bf16x8, ld_row16(dO + hoff, qrow, N, D, kc * 32 + 8 * g));
-    }
-    // Algorithm 1's preprocessing, fused: D_i = sum_c fl32(dO_ic O_ic) (BF16 x BF16
-    // products are exact in FP32), from this lane's column slices of the row,
-    // summed over the row's 4 lanes.  The key-major pass reads D back.
-    float dpart = 0.f;
+    for (int nb = 0; nb < 2; ++nb) {
+        const int qrow = q0w + nb * 16 + c16;
+        float dpart = 0.f;
 #pragma unroll
-    for (int kc = 0; kc < D / 32; ++kc) {
-        const u32x4 ow = ld_row16(O + hoff, qrow, N, D, kc * 32 + 8 * g);
-        const u32x4 uw = __builtin_bit_cast(u32x4, uf[kc]);
+        for (int kc = 0; kc < KC; ++kc) {
+            const u32x4 qw = ld_row16(Q + hoff, qrow, N, D, kc * 32 + 8 * g);
+            const u32x4 uw = ld_row16(dO + hoff, qrow, N, D, kc * 32 + 8 * g);
+            const u32x4 ow = ld_row16(O + hoff, qrow, N, D, kc * 32 + 8 * g);
+            qf[nb][kc] = __builtin_bit_cast(bf16x8, qw);
+            uf[nb][kc] = __builtin_bit_cast(bf16x8, uw);
+            // Algorithm 1's preprocessing, fused: D_i = sum_c fl32(dO_ic O_ic);
+            // BF16 x BF16 products are exact in FP32.
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            dpart += lo_bf16(uw[e]) * lo_bf16(ow[e]);
-            dpart += hi_bf16(uw[e]) * hi_bf16(ow[e]);
+            for (int e = 0; e < 4; ++e) {
+                dpart += lo_bf16(uw[e]) * lo_bf16(ow[e]);
+                dpart += hi_bf16(uw[e]) * hi_bf16(ow[e]);
+            }
         }
+        Di[nb] = xor_sum(dpart);
+        lse2[nb] = LSE[soff + min(qrow, N - 1)] * kLog2e;
     }
-    const float Di = xor_sum(dpart);
     const float c = scale * kLog2e;
-    const float lse2 = LSE[ridx] * kLog2e;
     const bf16x8 ones = ones_row0(c16);
 
-    f32x4 accA[D / 16], accB[GPROJ ? D / 16 : 1];
+    f32x4 accA[2][MB], accB[2][GPROJ ? MB : 1], accR[2], accM[2];
 #pragma unroll
-    for (int mb = 0; mb < D / 16; ++mb) accA[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nb = 0; nb < 2; ++nb) {
 #pragma unroll
-    for (int mb = 0; mb < (GPROJ ? D / 16 : 1); ++mb) accB[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    f32x4 accR = {0.f, 0.f, 0.f, 0.f}, accM = {0.f, 0.f, 0.f, 0.f};
+        for (int mb = 0; mb < MB; ++mb) accA[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int mb = 0; mb < (GPROJ ? MB : 1); ++mb) accB[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        accR[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        accM[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
 
     const int nkv = causal ? min(T, tile + 1) : T;
     const bool q_tail = tile * kTile + kTile > N;
 
-    TileStager<D, 2> st;
-    const uint16_t* const src[2] = {K + hoff, V + hoff};
-    st.fetch(src, 0, N, tid);
-    {
-        uint16_t* const dst[2] = {Ks[0], Vs[0]};
-        st.store(dst, tid);
-    }
+    TileDma<D> dma;
+    dma.init(tid);
+    dma.load(K + hoff, KV0[0], 0, N);
+    dma.load(V + hoff, KV0[1], 0, N);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    for (int kt = 0; kt < nkv; ++kt) {
+    // One key tile: compute on (Kc, Vc) while the DMA fills (Kn, Vn) with the
+    // next tile.
+    auto step = [&](int kt, const uint16_t* Kc, const uint16_t* Vc, uint16_t* Kn, uint16_t* Vn) {
         const int k0 = kt * kTile;
-        const int cur = kt & 1;
-        if (kt + 1 < nkv) st.fetch(src, k0 + kTile, N, tid);
-        const uint16_t* Kc = Ks[cur];
-        const uint16_t* Vc = Vs[cur];
+        if (kt + 1 < nkv) {
+            dma.load(K + hoff, Kn, k0 + kTile, N);
+            dma.load(V + hoff, Vn, k0 + kTile, N);
+        }
         const bool edge = (causal && kt == tile) || q_tail || k0 + kTile > N;
-
-        // Two halves of 32 keys.  S^T = K Q^T and dP^T = V dO^T leave each lane
-        // with keys 4g+i of each 16-key block for its own query.
+        // S^T = K Q^T and dP^T = V dO^T for this wave's 32 keys x 32 queries:
+        // s[nb][kb] holds keys 4g+i of key block kb for query block nb.
+        f32x4 s[2][2], dp[2][2];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            f32x4 s[2], dp[2];
+        for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-            for (int b = 0; b < 2; ++b) {
-                const int kb = 2 * h + b;
-                s[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-                dp[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int nb = 0; nb < 2; ++nb) {
+                s[nb][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+                dp[nb][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            }
 #pragma unroll
-                for (int kc = 0; kc < D / 32; ++kc) {
-                    s[b] = mfma_16x16x32(ld_b128(Kc + tile_off<D>(kb * 16 + c16, kc * 32 + 8 * g)),
-                                         qf[kc], s[b]);
-                    dp[b] = mfma_16x16x32(ld_b128(Vc + tile_off<D>(kb * 16 + c16, kc * 32 + 8 * g)),
-                                          uf[kc], dp[b]);
+            for (int kc = 0; kc < KC; ++kc) {
+                const int row = 32 * kh + kb * 16 + c16;
+                const bf16x8 ka = ld_b128(Kc + tile_off<D>(row, kc * 32 + 8 * g));
+                const bf16x8 va = ld_b128(Vc + tile_off<D>(row, kc * 32 + 8 * g));
+#pragma unroll
+                for (int nb = 0; nb < 2; ++nb) {
+                    s[nb][kb] = mfma_16x16x32(ka, qf[nb][kc], s[nb][kb]);
+                    dp[nb][kb] = mfma_16x16x32(va, uf[nb][kc], dp[nb][kb]);
                 }
             }
-            bf16x8 tf, rf;
-            if (edge)
-                dq_probs<true>(s, dp, c, lse2, Di, k0 + 32 * h, g, qrow, qok, N, causal, tf, rf);
-            else
-                dq_probs<false>(s, dp, c, lse2, Di, k0 + 32 * h, g, qrow, qok, N, causal, tf, rf);
-            // A^T[d][query] += K^T[d][key] t^T[key][query] (and B^T with r); the
-            // row sums rho, m come from a constant ones operand.
+        }
+        bf16x8 tf[2], rf[2];
 #pragma unroll
-            for (int mb = 0; mb < D / 16; ++mb) {
-                const bf16x8 ka = ld_tr_operand<D>(Kc, h * 32, mb * 16, c16, g);
-                accA[mb] = mfma_16x16x32(ka, tf, accA[mb]);
-                if (GPROJ) accB[mb] = mfma_16x16x32(ka, rf, accB[mb]);
-            }
-            if (GPROJ) {
-                accR = mfma_16x16x32(ones, tf, accR);
-                accM = mfma_16x16x32(ones, rf, accM);
+        for (int nb = 0; nb < 2; ++nb) {
+            const int qrow = q0w + nb * 16 + c16;
+            if (edge)
+                dq_probs<true>(s[nb], dp[nb], c, lse2[nb], Di[nb], k0 + 32 * kh, g, qrow, N,
+                               causal, tf[nb], rf[nb]);
+            else
+                dq_probs<false>(s[nb], dp[nb], c, lse2[nb], Di[nb], k0 + 32 * kh, g, qrow, N,
+                                causal, tf[nb], rf[nb]);
+        }
+        // A^T[d][query] += K^T[d][key] t^T[key][query] (and B^T with r); the
+        // row sums rho, m come from a constant ones operand.
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            const bf16x8 ka = ld_tr_operand<D>(Kc, 32 * kh, mb * 16, c16, g);
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb) {
+                accA[nb][mb] = mfma_16x16x32(ka, tf[nb], accA[nb][mb]);
+                if (GPROJ) accB[nb][mb] = mfma_16x16x32(ka, rf[nb], accB[nb][mb]);
             }
         }
-        if (kt + 1 < nkv) {
-            uint16_t* const dst[2] = {Ks[cur ^ 1], Vs[cur ^ 1]};
-            st.store(dst, tid);
+        if (GPROJ) {
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb) {
+                accR[nb] = mfma_16x16x32(ones, tf[nb], accR[nb]);
+                accM[nb] = mfma_16x16x32(ones, rf[nb], accM[nb]);
+            }
         }
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the next tile
         __syncthreads();
+    };
+    for (int kt = 0; kt < nkv; kt += 2) {
+        step(kt, KV0[0], KV0[1], KV1[0], KV1[1]);
+        if (kt + 1 < nkv) step(kt + 1, KV1[0], KV1[1], KV0[0], KV0[1]);
     }
 
-    // rho and m of this lane's query sit in accumulator row 0 (lanes g == 0).
-    float lam = 0.f, rho = 0.f, msum = 0.f;
-    if (GPROJ) {
-        rho = __shfl(accR[0], c16);
-        msum = __shfl(accM[0], c16);
-        lam = (msum != 0.f) ? rho / msum : 0.f;  // one IEEE FP32 division
-    }
-    if (qok) {
-        uint16_t* drow = dQ + hoff + (size_t)qrow * D;
+    // Add the partials of the two waves that own the same queries (one query
+    // block at a time, to bound the LDS the exchange needs).
+    float red[2][PER_NB];
 #pragma unroll
-        for (int mb = 0; mb < D / 16; ++mb) {
-            float v[4];
+    for (int nb = 0; nb < 2; ++nb) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
+                red[nb][(mb * 4 + i) * 2] = accA[nb][mb][i];
+                red[nb][(mb * 4 + i) * 2 + 1] = GPROJ ? accB[nb][mb][i] : 0.f;
+            }
+        red[nb][2 * MB * 4] = accR[nb][0];
+        red[nb][2 * MB * 4 + 1] = accM[nb][0];
+        if (nb) __syncthreads();  // the previous exchange has been read
+        pair_reduce<PER_NB, sizeof(KV0) / 4>(red[nb], reinterpret_cast<float*>(&KV0[0][0]), wave,
+                                             lane);
+    }
+    if (wave >= 2) return;
+
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+        const int qrow = q0w + nb * 16 + c16;
+        // rho and m of this lane's query sit in accumulator row 0 (lanes g == 0).
+        float lam = 0.f, rho = 0.f, msum = 0.f;
+        if (GPROJ) {
+            rho = __shfl(red[nb][2 * MB * 4], c16);
+            msum = __shfl(red[nb][2 * MB * 4 + 1], c16);
+            lam = (msum != 0.f) ? rho / msum : 0.f;  // one IEEE FP32 division
+        }
+        if (qrow < N) {
+            uint16_t* drow = dQ + hoff + (size_t)qrow * D;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+                float v[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
 #pragma clang fp contract(off)
-                if (GPROJ) {
-                    const float corr = lam * accB[mb][i];
-                    const float diff = accA[mb][i] - corr;
-                    v[i] = scale * diff;
-                } else {
-                    v[i] = scale * accA[mb][i];
+                    const float a = red[nb][(mb * 4 + i) * 2];
+                    const float b = red[nb][(mb * 4 + i) * 2 + 1];
+                    if (GPROJ) {
+                        const float corr = lam * b;
+                        const float diff = a - corr;
+                        v[i] = scale * diff;
+                    } else {
+                        v[i] = scale * a;
+                    }
+                }
+                st_bf16x4(drow + mb * 16 + 4 * g, v[0], v[1], v[2], v[3]);
+            }
+            if (WRITE_Z) {
+                // z = BF16(fl32(lambda q)) for the key correction: the lane holds
+                // d = kc*32 + 8g .. +7 of its query row.
+#pragma unroll
+                for (int kc = 0; kc < KC; ++kc) {
+                    bf16x8 z;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) z[e] = to_bf16(lam * bf16_to_f32(qf[nb][kc][e]));
+                    *reinterpret_cast<bf16x8*>(Zout + hoff + (size_t)qrow * D + kc * 32 + 8 * g) = z;
                 }
             }
-            st_bf16x4(drow + mb * 16 + 4 * g, v[0], v[1], v[2], v[3]);
-        }
-        if (WRITE_Z) {
-            // z = BF16(fl32(lambda q)) for the key correction: the lane holds
-            // d = kc*32 + 8g .. +7 of its query row.
-#pragma unroll
-            for (int kc = 0; kc < D / 32; ++kc) {
-                bf16x8 z;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) z[e] = to_bf16(lam * bf16_to_f32(qf[kc][e]));
-                *reinterpret_cast<bf16x8*>(Zout + hoff + (size_t)qrow * D + kc * 32 + 8 * g) = z;
+            if (g == 0) {
+                D_out[soff + qrow] = Di[nb];
+                rho_out[soff + qrow] = rho;
+                m_out[soff + qrow] = msum;
+                lam_out[soff + qrow] = lam;
             }
-        }
-        if (g == 0) {
-            D_out[ridx] = Di;
-            rho_out[ridx] = rho;
-            m_out[ridx] = msum;
-            lam_out[ridx] = lam;
         }
     }
 }
 
 // ----------------------------------------------------------- key-major pass
-// P, r, t for 32 queries (two 16-query blocks) of the key-major pass: lane
-// holds queries 4g+i of each block for its key.
+// P, r, t of one 16-key x 16-query block: s, dp hold queries 4g+i of the
+// block for this lane's key; they fill half `half` of the B operands tf, rf.
 template <bool MASK>
-__device__ __forceinline__ void dkdv_probs(const f32x4 (&s)[2], const f32x4 (&dp)[2],
-                                           const f32x4 (&l2)[2], const f32x4 (&dd)[2], float c,
-                                           int qb0, int g, int krow, int N, int causal,
-                                           bf16x8& tf, bf16x8& rf) {
+__device__ __forceinline__ void dkdv_probs(const f32x4& s, const f32x4& dp, const f32x4& l2,
+                                           const f32x4& dd, float c, int qb, int g, int krow,
+                                           int N, int causal, int half, bf16x8& tf, bf16x8& rf) {
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            float P = fexp2(fmaf(s[b][i], c, -l2[b][i]));
-            if constexpr (MASK) {
-                const int query = qb0 + b * 16 + 4 * g + i;
-                const bool ok = krow < N && query < N && (!causal || krow <= query);
-                P = ok ? P : 0.f;
-            }
-            tf[b * 4 + i] = to_bf16(P * (dp[b][i] - dd[b][i]));
-            rf[b * 4 + i] = to_bf16(P);
+    for (int i = 0; i < 4; ++i) {
+        float P = fexp2(fmaf(s[i], c, -l2[i]));
+        if constexpr (MASK) {
+            const int query = qb + 4 * g + i;
+            const bool ok = krow < N && query < N && (!causal || krow <= query);
+            P = ok ? P : 0.f;
         }
+        tf[half * 4 + i] = to_bf16(P * (dp[i] - dd[i]));
+        rf[half * 4 + i] = to_bf16(P);
+    }
+}
+
+// Four consecutive FP32 row statistics starting at row `row`, rows clamped to
+// N - 1 (tail rows are masked by the caller).  One 16-byte load when the four
+// rows exist and the address is 16-byte aligned.
+__device__ __forceinline__ f32x4 ld_stat4(const float* base, int row, int N) {
+    if (row + 3 < N && (reinterpret_cast<uintptr_t>(base + row) & 15) == 0)
+        return *reinterpret_cast<const f32x4*>(base + row);
+    f32x4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = base[min(row + i, N - 1)];
+    return v;
 }
 
 template <int D, bool GPROJ>
@@ -290,10 +348,15 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     const float* __restrict__ LSE, const float* __restrict__ Drow,
     const uint16_t* __restrict__ Z, uint16_t* __restrict__ dK, uint16_t* __restrict__ dV,
     int BH, int N, int causal, float scale) {
+    constexpr int MB = D / 16;
+    constexpr int KC = D / 32;
     constexpr int NT = GPROJ ? 3 : 2;  // staged tensors: Q, dO (and Z = BF16(lambda Q))
-    __shared__ __attribute__((aligned(16))) uint16_t Ts[2][NT][kTile * D];
-    __shared__ __attribute__((aligned(16))) float lse2s[2][kTile];
-    __shared__ __attribute__((aligned(16))) float Ds[2][kTile];
+    constexpr int NV = GPROJ ? 3 : 2;  // accumulators per output element: dV, dK^acc (, C)
+    constexpr int PER_KB = NV * MB * 4;
+    // Query tiles, double-buffered in two separate LDS objects so the compiler
+    // can tell the tile being read from the one the DMA is filling.
+    __shared__ __attribute__((aligned(16))) uint16_t T0[NT][kTile * D];
+    __shared__ __attribute__((aligned(16))) uint16_t T1[NT][kTile * D];
 
     const int T = (N + kTile - 1) / kTile;
     int bh, tile;
@@ -303,126 +366,167 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
-    const int krow = tile * kTile + wave * 16 + c16;
-    const bool kok = krow < N;
+    const int kh = wave & 1;   // which 32 of the workgroup's 64 keys
+    const int qh = wave >> 1;  // which 32 of each 64-query tile
+    const int k0w = tile * kTile + 32 * kh;
 
-    // K^T and V^T as B operands: column = this lane's key, k = d.
-    bf16x8 kf[D / 32], vf[D / 32];
+    // K^T and V^T as B operands: column = this lane's key of block kb, k = d.
+    bf16x8 kf[2][KC], vf[2][KC];
 #pragma unroll
-    for (int kc = 0; kc < D / 32; ++kc) {
-        kf[kc] = __builtin_bit_cast(bf16x8, ld_row16(K + hoff, krow, N, D, kc * 32 + 8 * g));
-        vf[kc] = __builtin_bit_cast(bf16x8, ld_row16(V + hoff, krow, N, D, kc * 32 + 8 * g));
-    }
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int kc = 0; kc < KC; ++kc) {
+            const int krow = k0w + kb * 16 + c16;
+            kf[kb][kc] = __builtin_bit_cast(bf16x8, ld_row16(K + hoff, krow, N, D, kc * 32 + 8 * g));
+            vf[kb][kc] = __builtin_bit_cast(bf16x8, ld_row16(V + hoff, krow, N, D, kc * 32 + 8 * g));
+        }
     const float c = scale * kLog2e;
 
-    f32x4 accV[D / 16], accK[D / 16], accC[GPROJ ? D / 16 : 1];
+    f32x4 accV[2][MB], accK[2][MB], accC[2][GPROJ ? MB : 1];
 #pragma unroll
-    for (int mb = 0; mb < D / 16; ++mb) {
-        accV[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-        accK[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            accV[kb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            accK[kb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int mb = 0; mb < (GPROJ ? MB : 1); ++mb) accC[kb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-#pragma unroll
-    for (int mb = 0; mb < (GPROJ ? D / 16 : 1); ++mb) accC[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     const int qt0 = causal ? tile : 0;
     const bool k_tail = tile * kTile + kTile > N;
-
-    TileStager<D, NT> st;
     const uint16_t* src[NT];
     src[0] = Q + hoff;
     src[1] = dO + hoff;
     if (GPROJ) src[NT - 1] = Z + hoff;
-    float lse_reg = 0.f, d_reg = 0.f;
-    auto fetch_stats = [&](int q0) {
-        if (tid < kTile) {
-            const int row = min(q0 + tid, N - 1);
-            lse_reg = LSE[soff + row];
-            d_reg = Drow[soff + row];
-        }
-    };
-    auto store = [&](int buf) {
-        uint16_t* dst[NT];
+
+    TileDma<D> dma;
+    dma.init(tid);
+    auto load_tile = [&](uint16_t (*dst)[kTile * D], int q0) {
 #pragma unroll
-        for (int t = 0; t < NT; ++t) dst[t] = Ts[buf][t];
-        st.store(dst, tid);
-        if (tid < kTile) {
-            lse2s[buf][tid] = lse_reg * kLog2e;
-            Ds[buf][tid] = d_reg;
-        }
+        for (int t = 0; t < NT; ++t) dma.load(src[t], dst[t], q0, N);
     };
-    st.fetch(src, qt0 * kTile, N, tid);
-    fetch_stats(qt0 * kTile);
-    store(0);
+    load_tile(T0, qt0 * kTile);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    for (int qt = qt0; qt < T; ++qt) {
+
+    // One query tile: compute on `cur` while the DMA fills `nxt` with the next.
+    auto step = [&](int qt, uint16_t (*cur)[kTile * D], uint16_t (*nxt)[kTile * D]) {
         const int q0 = qt * kTile;
-        const int cur = (qt - qt0) & 1;
-        if (qt + 1 < T) {
-            st.fetch(src, q0 + kTile, N, tid);
-            fetch_stats(q0 + kTile);
+        // Row statistics of this wave's 32 queries, straight from global memory
+        // (issued before the DMA so the wait for them does not cover it).
+        f32x4 l2[2], dd[2];
+#pragma unroll
+        for (int mq = 0; mq < 2; ++mq) {
+            const int qr = q0 + 32 * qh + mq * 16 + 4 * g;
+            l2[mq] = ld_stat4(LSE + soff, qr, N);
+            dd[mq] = ld_stat4(Drow + soff, qr, N);
         }
-        const uint16_t* Qc = Ts[cur][0];
-        const uint16_t* Uc = Ts[cur][1];
-        const uint16_t* Zc = Ts[cur][NT - 1];
+        if (qt + 1 < T) load_tile(nxt, q0 + kTile);
+        const uint16_t* Qc = cur[0];
+        const uint16_t* Uc = cur[1];
+        const uint16_t* Zc = cur[NT - 1];
         const bool edge = (causal && qt == tile) || k_tail || q0 + kTile > N;
 
-        // Two halves of 32 queries.  S = Q K^T and dP = dO V^T leave each lane
-        // with queries 4g+i of each 16-query block for its own key.
+        // S = Q K^T and dP = dO V^T for this wave's 32 queries x 32 keys, one
+        // 16 x 16 block at a time: s holds queries 4g+i of query block mq for
+        // key block kb, and P, r, t of that block go straight into half mq of
+        // the key block's B operands tf[kb], rf[kb].
+        bf16x8 tf[2], rf[2];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            f32x4 s[2], dp[2], l2[2], dd[2];
+        for (int mq = 0; mq < 2; ++mq) {
+            const int row = 32 * qh + mq * 16 + c16;
+            bf16x8 qa[KC], ua[KC];
 #pragma unroll
-            for (int b = 0; b < 2; ++b) {
-                const int mq = 2 * h + b;
-                s[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-                dp[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int kc = 0; kc < D / 32; ++kc) {
-                    s[b] = mfma_16x16x32(ld_b128(Qc + tile_off<D>(mq * 16 + c16, kc * 32 + 8 * g)),
-                                         kf[kc], s[b]);
-                    dp[b] = mfma_16x16x32(ld_b128(Uc + tile_off<D>(mq * 16 + c16, kc * 32 + 8 * g)),
-                                          vf[kc], dp[b]);
-                }
-                l2[b] = *reinterpret_cast<const f32x4*>(&lse2s[cur][mq * 16 + 4 * g]);
-                dd[b] = *reinterpret_cast<const f32x4*>(&Ds[cur][mq * 16 + 4 * g]);
+            for (int kc = 0; kc < KC; ++kc) {
+                qa[kc] = ld_b128(Qc + tile_off<D>(row, kc * 32 + 8 * g));
+                ua[kc] = ld_b128(Uc + tile_off<D>(row, kc * 32 + 8 * g));
             }
-            bf16x8 tf, rf;
-            if (edge)
-                dkdv_probs<true>(s, dp, l2, dd, c, q0 + 32 * h, g, krow, N, causal, tf, rf);
-            else
-                dkdv_probs<false>(s, dp, l2, dd, c, q0 + 32 * h, g, krow, N, causal, tf, rf);
-            // dV^T[dv][key] += dO^T r ; dK^T += Q^T t ; C^T += Z^T r.
+            const f32x4 l2m = l2[mq] * kLog2e;
 #pragma unroll
-            for (int mb = 0; mb < D / 16; ++mb) {
-                accV[mb] = mfma_16x16x32(ld_tr_operand<D>(Uc, h * 32, mb * 16, c16, g), rf, accV[mb]);
-                accK[mb] = mfma_16x16x32(ld_tr_operand<D>(Qc, h * 32, mb * 16, c16, g), tf, accK[mb]);
-                if (GPROJ)
-                    accC[mb] = mfma_16x16x32(ld_tr_operand<D>(Zc, h * 32, mb * 16, c16, g), rf,
-                                             accC[mb]);
+            for (int kb = 0; kb < 2; ++kb) {
+                f32x4 sv = {0.f, 0.f, 0.f, 0.f}, dpv = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int kc = 0; kc < KC; ++kc) {
+                    sv = mfma_16x16x32(qa[kc], kf[kb][kc], sv);
+                    dpv = mfma_16x16x32(ua[kc], vf[kb][kc], dpv);
+                }
+                const int krow = k0w + kb * 16 + c16;
+                const int qb = q0 + 32 * qh + mq * 16;
+                if (edge)
+                    dkdv_probs<true>(sv, dpv, l2m, dd[mq], c, qb, g, krow, N, causal, mq, tf[kb], rf[kb]);
+                else
+                    dkdv_probs<false>(sv, dpv, l2m, dd[mq], c, qb, g, krow, N, causal, mq, tf[kb], rf[kb]);
             }
         }
-        if (qt + 1 < T) store(cur ^ 1);
+        // dV^T[dv][key] += dO^T r ; dK^T += Q^T t ; C^T += Z^T r.
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            const bf16x8 ua = ld_tr_operand<D>(Uc, 32 * qh, mb * 16, c16, g);
+            const bf16x8 qa = ld_tr_operand<D>(Qc, 32 * qh, mb * 16, c16, g);
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+                accV[kb][mb] = mfma_16x16x32(ua, rf[kb], accV[kb][mb]);
+                accK[kb][mb] = mfma_16x16x32(qa, tf[kb], accK[kb][mb]);
+            }
+            if (GPROJ) {
+                const bf16x8 za = ld_tr_operand<D>(Zc, 32 * qh, mb * 16, c16, g);
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb) accC[kb][mb] = mfma_16x16x32(za, rf[kb], accC[kb][mb]);
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the next tile
         __syncthreads();
+    };
+    for (int qt = qt0; qt < T; qt += 2) {
+        step(qt, T0, T1);
+        if (qt + 1 < T) step(qt + 1, T1, T0);
     }
 
-    if (kok) {
+    // Add the partials of the two waves that own the same keys (one key block
+    // at a time, to bound the LDS the exchange needs).
+    float red[2][PER_KB];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int j = (mb * 4 + i) * NV;
+                red[kb][j] = accV[kb][mb][i];
+                red[kb][j + 1] = accK[kb][mb][i];
+                if (GPROJ) red[kb][j + NV - 1] = accC[kb][mb][i];
+            }
+        if (kb) __syncthreads();  // the previous exchange has been read
+        pair_reduce<PER_KB, sizeof(T0) / 4>(red[kb], reinterpret_cast<float*>(&T0[0][0]), wave,
+                                             lane);
+    }
+    if (wave >= 2) return;
+
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+        const int krow = k0w + kb * 16 + c16;
+        if (krow >= N) continue;
         uint16_t* vrow = dV + hoff + (size_t)krow * D;
         uint16_t* krw = dK + hoff + (size_t)krow * D;
 #pragma unroll
-        for (int mb = 0; mb < D / 16; ++mb) {
-            st_bf16x4(vrow + mb * 16 + 4 * g, accV[mb][0], accV[mb][1], accV[mb][2], accV[mb][3]);
-            float v[4];
+        for (int mb = 0; mb < MB; ++mb) {
+            float dv[4], dk[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
 #pragma clang fp contract(off)
+                const int j = (mb * 4 + i) * NV;
+                dv[i] = red[kb][j];
                 if (GPROJ) {
-                    const float diff = accK[mb][i] - accC[mb][i];
-                    v[i] = scale * diff;
+                    const float diff = red[kb][j + 1] - red[kb][j + NV - 1];
+                    dk[i] = scale * diff;
                 } else {
-                    v[i] = scale * accK[mb][i];
+                    dk[i] = scale * red[kb][j + 1];
                 }
             }
-            st_bf16x4(krw + mb * 16 + 4 * g, v[0], v[1], v[2], v[3]);
+            st_bf16x4(vrow + mb * 16 + 4 * g, dv[0], dv[1], dv[2], dv[3]);
+            st_bf16x4(krw + mb * 16 + 4 * g, dk[0], dk[1], dk[2], dk[3]);
         }
     }
 }
@@ -435,7 +539,7 @@ hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V
                          int mode, const Shape& s, hipStream_t st) {
     const int T = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
-#define GPA_DQ(DD, GP, WZ)                                                                  \
+#define GPA_DQ(DD, GP, WZ)                                                                      \
     bwd_dq_kernel<DD, GP, WZ><<<grid, block, 0, st>>>(Q, K, V, O, dO, LSE, Drow, dQ, rho, msum, \
                                                       lambda, Z, s.BH, s.N, s.causal, s.scale)
     if (s.d == 64) {

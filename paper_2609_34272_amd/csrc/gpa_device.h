@@ -54,6 +54,47 @@ __device__ __forceinline__ int tile_off(int r, int col) {
     return r * D + (((col >> 3) ^ swz(r)) << 3) + (col & 7);
 }
 
+// Direct global -> LDS staging of one 64-row tile with the gfx950 LDS DMA load
+// (global_load_lds_dwordx4): lane L of a wave writes 16 bytes at M0 + 16 L,
+// so each wave call fills a contiguous 1 KB of the swizzled tile and every
+// lane loads the global chunk that the swizzle places in its slot.  No
+// registers or LDS write instructions are involved; completion is tracked by
+// vmcnt.  Rows at or beyond N are loaded from row N-1 instead (finite data that
+// the tail-tile masks zero out), so no load leaves the tensor.
+template <int D>
+struct TileDma {
+    static constexpr int CALLS = kTile * D * 2 / (kThreads * 16);
+    int row[CALLS];   // tile row of this lane's chunk in call k
+    int col[CALLS];   // logical column of that chunk
+    int lds[CALLS];   // byte offset of this wave's 1 KB block (wave-uniform)
+
+    __device__ __forceinline__ void init(int tid) {
+        const int lane = tid & 63, wave = tid >> 6;
+#pragma unroll
+        for (int k = 0; k < CALLS; ++k) {
+            const int b = (k * 4 + wave) * 1024 + 16 * lane;
+            const int r = b / (2 * D);
+            const int p = (b - r * 2 * D) / 16;
+            row[k] = r;
+            col[k] = (p ^ swz(r)) * 8;
+            lds[k] = (k * 4 + wave) * 1024;
+        }
+    }
+    __device__ __forceinline__ void load(const uint16_t* src, uint16_t* dst, int row0,
+                                         int N) const {
+        const bool full = row0 + kTile <= N;
+#pragma unroll
+        for (int k = 0; k < CALLS; ++k) {
+            int r = row0 + row[k];
+            if (!full) r = r < N ? r : N - 1;
+            const uint16_t* gp = src + (size_t)r * D + col[k];
+            __builtin_amdgcn_global_load_lds(
+                (const __attribute__((address_space(1))) void*)gp,
+                (__attribute__((address_space(3))) void*)((char*)dst + lds[k]), 16, 0, 0);
+        }
+    }
+};
+
 // Transposed MFMA operand read straight from a row-major LDS tile X[k][n]
 // with the gfx950 LDS transpose load ds_read_b64_tr_b16.  Within each 16-lane
 // group, that instruction hands lane j element j of the 4 x 16 block formed by
@@ -156,7 +197,7 @@ __device__ __forceinline__ void map_block(int bid, int BH, int T, bool heavy_hig
 #define GPA_FWD_OCC 2
 #endif
 #ifndef GPA_DQ_OCC64
-#define GPA_DQ_OCC64 3
+#define GPA_DQ_OCC64 2
 #endif
 #ifndef GPA_DKDV_OCC64
 #define GPA_DKDV_OCC64 2

@@ -4,13 +4,17 @@
 // unscaled running row maximum xmax, so the largest logit maps to exactly
 // exp2(0) = 1.
 //
-// Schedule: one workgroup per (batch*head, 64-query tile); 4 waves, each owning
-// 16 queries.  K and V tiles of 64 keys are staged row-major in LDS (V is read
-// back transposed with the LDS transpose load).  A wave computes S^T = K Q^T with v_mfma_f32_16x16x32_bf16, so
-// each lane holds 16 logits of ONE query (its column): the row maximum and the
-// row sum are in-lane except for a 4-way exchange.  The probabilities are then
-// already in the B-operand layout of O^T += V^T P^T, whose accumulator again
-// keeps one query per lane, so the online-softmax rescale is a per-lane scalar.
+// Schedule: one workgroup per (batch*head, 64-query tile); 4 waves.  Wave w
+// owns 32 of the 64 queries (two 16-query MFMA blocks sharing every LDS
+// fragment) and half of each 64-key tile; the two waves with the same queries
+// merge their online-softmax states at the end with the same rescale rule.  K
+// and V tiles are loaded straight into LDS (row-major, swizzled, double
+// buffered); V is read back transposed with the LDS transpose load.  A wave
+// computes S^T = K Q^T with v_mfma_f32_16x16x32_bf16, so each lane holds the
+// logits of ONE query (its column): the row maximum and sum are in-lane except
+// for a 4-way exchange.  The probabilities are then already in the B-operand
+// layout of O^T += V^T P^T, whose accumulator again keeps one query per lane,
+// so the online-softmax rescale is a per-lane scalar.
 #include "gpa_device.h"
 #include "gpa_launch.h"
 
@@ -22,9 +26,13 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, uint16_t* __restrict__ O, float* __restrict__ LSE,
     int BH, int N, int causal, float scale) {
-    constexpr int CH = kTile * D / 8 / kThreads;
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[kTile * D];
-    __shared__ __attribute__((aligned(16))) uint16_t Vs[kTile * D];
+    constexpr int MB = D / 16;
+    constexpr int KC = D / 32;
+    constexpr int PER_NB = MB * 4 + 2;  // acc, m, l of one query block
+    // K and V tiles, double-buffered in two separate LDS objects so the
+    // compiler can tell the tile being read from the one the DMA is filling.
+    __shared__ __attribute__((aligned(16))) uint16_t KV0[2][kTile * D];
+    __shared__ __attribute__((aligned(16))) uint16_t KV1[2][kTile * D];
 
     const int T = (N + kTile - 1) / kTile;
     int bh, tile;
@@ -33,117 +41,163 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
-    const int qrow = tile * kTile + wave * 16 + c16;
-    const bool qok = qrow < N;
+    const int qh = wave & 1;   // which 32 of the workgroup's 64 queries
+    const int kh = wave >> 1;  // which 32 of each 64-key tile
+    const int q0w = tile * kTile + 32 * qh;
 
-    // Q^T as the B operand: column = this lane's query, k = d.
-    bf16x8 qf[D / 32];
+    // Q^T as the B operand: column = this lane's query of block nb, k = d.
+    bf16x8 qf[2][KC];
 #pragma unroll
-    for (int kc = 0; kc < D / 32; ++kc)
-        qf[kc] = __builtin_bit_cast(bf16x8, ld_row16(Q + hoff, qrow, N, D, kc * 32 + 8 * g));
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int kc = 0; kc < KC; ++kc)
+            qf[nb][kc] = __builtin_bit_cast(
+                bf16x8, ld_row16(Q + hoff, q0w + nb * 16 + c16, N, D, kc * 32 + 8 * g));
 
     const float c = scale * kLog2e;  // fl32(alpha log2 e)
-    float mrun = -INFINITY;          // running maximum of the unscaled logits
-    float lrun = 0.f;                // this lane's share of the running sum of z
-    f32x4 acc[D / 16];
+    float mrun[2] = {-INFINITY, -INFINITY};  // running maximum of the unscaled logits
+    float lrun[2] = {0.f, 0.f};              // this lane's share of the running sum of z
+    f32x4 acc[2][MB];                        // O^T[dv][query]
 #pragma unroll
-    for (int mb = 0; mb < D / 16; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     const int kv_end = causal ? min(N, (tile + 1) * kTile) : N;
     const int nkv = (kv_end + kTile - 1) / kTile;
 
-    u32x4 kreg[CH], vreg[CH];
-    auto fetch = [&](int k0) {
-#pragma unroll
-        for (int cI = 0; cI < CH; ++cI) {
-            const int ch = tid + cI * kThreads;
-            const int r = ch / (D / 8);
-            const int cc = (ch - r * (D / 8)) * 8;
-            kreg[cI] = ld_row16(K + hoff, k0 + r, N, D, cc);
-            vreg[cI] = ld_row16(V + hoff, k0 + r, N, D, cc);
-        }
-    };
-    fetch(0);
-    for (int kt = 0; kt < nkv; ++kt) {
-        const int k0 = kt * kTile;
-        __syncthreads();
-#pragma unroll
-        for (int cI = 0; cI < CH; ++cI) {
-            const int ch = tid + cI * kThreads;
-            const int r = ch / (D / 8);
-            const int cc = (ch - r * (D / 8)) * 8;
-            *reinterpret_cast<u32x4*>(Ks + tile_off<D>(r, cc)) = kreg[cI];
-            *reinterpret_cast<u32x4*>(Vs + tile_off<D>(r, cc)) = vreg[cI];
-        }
-        __syncthreads();
-        if (kt + 1 < nkv) fetch(k0 + kTile);
+    TileDma<D> dma;
+    dma.init(tid);
+    dma.load(K + hoff, KV0[0], 0, N);
+    dma.load(V + hoff, KV0[1], 0, N);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
 
-        // S^T[key][query] for 4 blocks of 16 keys.
-        f32x4 s[4];
+    auto step = [&](int kt, const uint16_t* Kc, const uint16_t* Vc, uint16_t* Kn, uint16_t* Vn) {
+        const int k0 = kt * kTile;
+        if (kt + 1 < nkv) {
+            dma.load(K + hoff, Kn, k0 + kTile, N);
+            dma.load(V + hoff, Vn, k0 + kTile, N);
+        }
+        // S^T[key][query] for this wave's 32 keys x 32 queries; s[nb][kb]
+        // holds keys 4g+i of key block kb for query block nb.
+        f32x4 s[2][2];
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-            s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int kb = 0; kb < 2; ++kb) {
+            s[0][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            s[1][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int kc = 0; kc < D / 32; ++kc)
-                s[kb] = mfma_16x16x32(ld_b128(Ks + tile_off<D>(kb * 16 + c16, kc * 32 + 8 * g)), qf[kc],
-                                      s[kb]);
+            for (int kc = 0; kc < KC; ++kc) {
+                const bf16x8 ka = ld_b128(Kc + tile_off<D>(32 * kh + kb * 16 + c16, kc * 32 + 8 * g));
+#pragma unroll
+                for (int nb = 0; nb < 2; ++nb) s[nb][kb] = mfma_16x16x32(ka, qf[nb][kc], s[nb][kb]);
+            }
         }
         // Only the diagonal tile and the key tail need masks (uniform branch).
         if ((causal && kt == tile) || k0 + kTile > N) {
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+            for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int key = k0 + kb * 16 + 4 * g + i;
-                    const bool ok = key < N && (!causal || key <= qrow);
-                    s[kb][i] = ok ? s[kb][i] : -INFINITY;
-                }
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int key = k0 + 32 * kh + kb * 16 + 4 * g + i;
+                        const int qrow = q0w + nb * 16 + c16;
+                        const bool ok = key < N && (!causal || key <= qrow);
+                        s[nb][kb][i] = ok ? s[nb][kb][i] : -INFINITY;
+                    }
         }
-        float mx = s[0][0];
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[kb][i]);
-        mx = xor_max(mx);
-        const float mnew = fmaxf(mrun, mx);
-        // Rescale by exp2(fl32[fl32(mold - mnew) * c]): the same rule as z.
-        // (mnew is finite: key 0 is visible to every row in tile 0.)
-        const float corr = fexp2((mrun - mnew) * c);
-        lrun *= corr;
-#pragma unroll
-        for (int mb = 0; mb < D / 16; ++mb) acc[mb] *= corr;
-
         bf16x8 pf[2];
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
+        for (int nb = 0; nb < 2; ++nb) {
+            float mx = s[nb][0][0];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float z = fexp2((s[kb][i] - mnew) * c);
-                lrun += z;
-                pf[kb >> 1][(kb & 1) * 4 + i] = to_bf16(z);
-            }
-        mrun = mnew;
-
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[nb][kb][i]);
+            mx = xor_max(mx);
+            const float mnew = fmaxf(mrun[nb], mx);
+            // A wave half may not have seen a visible key yet (mnew = -inf);
+            // then every z is 0 and nothing is rescaled.
+            const float ms = (mnew == -INFINITY) ? 0.f : mnew;
+            // Rescale by exp2(fl32[fl32(mold - mnew) * c]): the same rule as z.
+            const float corr = fexp2((mrun[nb] - ms) * c);
+            lrun[nb] *= corr;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) acc[nb][mb] *= corr;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float z = fexp2((s[nb][kb][i] - ms) * c);
+                    lrun[nb] += z;
+                    pf[nb][kb * 4 + i] = to_bf16(z);
+                }
+            mrun[nb] = mnew;
+        }
         // O^T[dv][query] += V^T[dv][key] P^T[key][query].
 #pragma unroll
-        for (int mb = 0; mb < D / 16; ++mb)
+        for (int mb = 0; mb < MB; ++mb) {
+            const bf16x8 va = ld_tr_operand<D>(Vc, 32 * kh, mb * 16, c16, g);
 #pragma unroll
-            for (int kc2 = 0; kc2 < 2; ++kc2)
-                acc[mb] = mfma_16x16x32(ld_tr_operand<D>(Vs, kc2 * 32, mb * 16, c16, g), pf[kc2],
-                                        acc[mb]);
+            for (int nb = 0; nb < 2; ++nb) acc[nb][mb] = mfma_16x16x32(va, pf[nb], acc[nb][mb]);
+        }
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the next tile
+        __syncthreads();
+    };
+    for (int kt = 0; kt < nkv; kt += 2) {
+        step(kt, KV0[0], KV0[1], KV1[0], KV1[1]);
+        if (kt + 1 < nkv) step(kt + 1, KV1[0], KV1[1], KV0[0], KV0[1]);
     }
 
-    const float ltot = xor_sum(lrun);
-    if (qok) {
-        uint16_t* orow = O + hoff + (size_t)qrow * D;
+    // Merge the two key halves of each query (waves w and w + 2): waves 2, 3
+    // park (acc, m, l) in LDS, waves 0, 1 combine them with the same rescale
+    // rule and finish.
+    // Query block nb goes through buffer object nb (each holds 2 x 64 x PER_NB
+    // floats).
+    static_assert(sizeof(KV0) >= 2 * 64 * PER_NB * sizeof(float), "merge space");
+    float* const scratch[2] = {reinterpret_cast<float*>(&KV0[0][0]),
+                               reinterpret_cast<float*>(&KV1[0][0])};
+    if (wave >= 2) {
 #pragma unroll
-        for (int mb = 0; mb < D / 16; ++mb)
-            st_bf16x4(orow + mb * 16 + 4 * g, acc[mb][0] / ltot, acc[mb][1] / ltot,
-                      acc[mb][2] / ltot, acc[mb][3] / ltot);
-        if (g == 0) {
+        for (int nb = 0; nb < 2; ++nb) {
+            float* p = scratch[nb] + (wave - 2) * 64 * PER_NB + lane;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) p[(mb * 4 + i) * 64] = acc[nb][mb][i];
+            p[(MB * 4) * 64] = mrun[nb];
+            p[(MB * 4 + 1) * 64] = lrun[nb];
+        }
+    }
+    __syncthreads();
+    if (wave >= 2) return;
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+        const float* p = scratch[nb] + wave * 64 * PER_NB + lane;
+        const float mo = p[(MB * 4) * 64];
+        const float lo = p[(MB * 4 + 1) * 64];
+        const float mt = fmaxf(mrun[nb], mo);
+        const float ms = (mt == -INFINITY) ? 0.f : mt;
+        const float fa = fexp2((mrun[nb] - ms) * c);
+        const float fb = fexp2((mo - ms) * c);
+        const float ltot = xor_sum(lrun[nb] * fa + lo * fb);
+        const int qrow = q0w + nb * 16 + c16;
+        if (qrow < N) {
+            uint16_t* orow = O + hoff + (size_t)qrow * D;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+                float v[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    v[i] = (acc[nb][mb][i] * fa + p[(mb * 4 + i) * 64] * fb) / ltot;
+                st_bf16x4(orow + mb * 16 + 4 * g, v[0], v[1], v[2], v[3]);
+            }
+            if (g == 0) {
 #pragma clang fp contract(off)
-            const float lse = scale * mrun + logf(ltot);
-            LSE[(size_t)bh * N + qrow] = lse;
+                const float lse = scale * mt + logf(ltot);
+                LSE[(size_t)bh * N + qrow] = lse;
+            }
         }
     }
 }
