@@ -40,6 +40,8 @@
 #include "gpa_device.h"
 #include "gpa_launch.h"
 
+#include <type_traits>
+
 namespace gpa {
 namespace {
 
@@ -84,7 +86,7 @@ __device__ __forceinline__ void dq_probs(const f32x4 (&s)[2], const f32x4 (&dp)[
             float P = fexp2(fmaf(s[kb][i], c, -lse2));
             if constexpr (MASK) {
                 const int key = key0 + kb * 16 + 4 * g + i;
-                const bool ok = qrow < N && key < N && (!causal || key <= qrow);
+                const bool ok = key < N && (!causal || key <= qrow);
                 P = ok ? P : 0.f;
             }
             tf[kb * 4 + i] = to_bf16(P * (dp[kb][i] - Di));
@@ -97,9 +99,9 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, const uint16_t* __restrict__ O,
     const uint16_t* __restrict__ dO, const float* __restrict__ LSE, float* __restrict__ D_out,
-    uint16_t* __restrict__ dQ, float* __restrict__ rho_out, float* __restrict__ m_out,
-    float* __restrict__ lam_out, uint16_t* __restrict__ Zout, int BH, int N, int causal,
-    float scale) {
+    float* __restrict__ L2p, float* __restrict__ Dp, uint16_t* __restrict__ dQ,
+    float* __restrict__ rho_out, float* __restrict__ m_out, float* __restrict__ lam_out,
+    uint16_t* __restrict__ Zout, int BH, int N, int causal, float scale) {
     constexpr int MB = D / 16;  // 16-column blocks of d
     constexpr int KC = D / 32;  // 32-wide k chunks of d
     constexpr int PER_NB = 2 * MB * 4 + 2;  // partial A, B (interleaved) and rho, m
@@ -111,18 +113,25 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     __shared__ __attribute__((aligned(16))) uint16_t KV1[2][kTile * D];  // [K, V], buffer 1
 
     const int T = (N + kTile - 1) / kTile;
+    const int Np = T * kTile;
     int bh, tile;
     map_block(blockIdx.x, BH, T, causal != 0, &bh, &tile);
     const size_t hoff = (size_t)bh * N * D;
     const size_t soff = (size_t)bh * N;
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, c16 = lane & 15;
     const int qh = wave & 1;   // which 32 of the workgroup's 64 queries
     const int kh = wave >> 1;  // which 32 of each 64-key tile
     const int q0w = tile * kTile + 32 * qh;
 
     // Q^T and dO^T as B operands: column = this lane's query of block nb, k = d.
+    // Rows beyond N load as zero.
+    const uint32_t tbytes = (uint32_t)N * (2 * D);
+    const rsrc_t rq = make_rsrc(Q + hoff, tbytes);
+    const rsrc_t ru = make_rsrc(dO + hoff, tbytes);
+    const rsrc_t ro = make_rsrc(O + hoff, tbytes);
     bf16x8 qf[2][KC], uf[2][KC];
     float lse2[2], Di[2];
 #pragma unroll
@@ -131,9 +140,9 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
         float dpart = 0.f;
 #pragma unroll
         for (int kc = 0; kc < KC; ++kc) {
-            const u32x4 qw = ld_row16(Q + hoff, qrow, N, D, kc * 32 + 8 * g);
-            const u32x4 uw = ld_row16(dO + hoff, qrow, N, D, kc * 32 + 8 * g);
-            const u32x4 ow = ld_row16(O + hoff, qrow, N, D, kc * 32 + 8 * g);
+            const u32x4 qw = ld_row16<D>(rq, qrow, kc * 32 + 8 * g);
+            const u32x4 uw = ld_row16<D>(ru, qrow, kc * 32 + 8 * g);
+            const u32x4 ow = ld_row16<D>(ro, qrow, kc * 32 + 8 * g);
             qf[nb][kc] = __builtin_bit_cast(bf16x8, qw);
             uf[nb][kc] = __builtin_bit_cast(bf16x8, uw);
             // Algorithm 1's preprocessing, fused: D_i = sum_c fl32(dO_ic O_ic);
@@ -145,7 +154,8 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
             }
         }
         Di[nb] = xor_sum(dpart);
-        lse2[nb] = LSE[soff + min(qrow, N - 1)] * kLog2e;
+        // Rows beyond N get log2-LSE = +inf, so every P of theirs is exactly 0.
+        lse2[nb] = qrow < N ? LSE[soff + qrow] * kLog2e : INFINITY;
     }
     const float c = scale * kLog2e;
     const bf16x8 ones = ones_row0(c16);
@@ -162,23 +172,41 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     }
 
     const int nkv = causal ? min(T, tile + 1) : T;
-    const bool q_tail = tile * kTile + kTile > N;
+    // Only the last key tile can need masks: the diagonal tile (causal) or the
+    // key tail (N not a multiple of the tile).  Query rows beyond N need none
+    // (their P is 0 and they are not stored).
+    const int nplain = (causal || (N % kTile)) ? nkv - 1 : nkv;
+
+    // Rows beyond N are never written by the DMA: zero both buffers once so
+    // every value a product can read is finite.
+    {
+        u32x4* z0 = reinterpret_cast<u32x4*>(&KV0[0][0]);
+        u32x4* z1 = reinterpret_cast<u32x4*>(&KV1[0][0]);
+        constexpr int n16 = (int)(sizeof(KV0) / 16);
+#pragma unroll
+        for (int i = tid; i < n16; i += kThreads) {
+            z0[i] = u32x4{0u, 0u, 0u, 0u};
+            z1[i] = u32x4{0u, 0u, 0u, 0u};
+        }
+    }
+    __syncthreads();
 
     TileDma<D> dma;
-    dma.init(tid);
+    dma.init(lane, wave);
     dma.load(K + hoff, KV0[0], 0, N);
     dma.load(V + hoff, KV0[1], 0, N);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     // One key tile: compute on (Kc, Vc) while the DMA fills (Kn, Vn) with the
     // next tile.
-    auto step = [&](int kt, const uint16_t* Kc, const uint16_t* Vc, uint16_t* Kn, uint16_t* Vn) {
+    auto step = [&](auto masked, int kt, const uint16_t* Kc, const uint16_t* Vc, uint16_t* Kn,
+                    uint16_t* Vn) {
+        constexpr bool MASK = decltype(masked)::value;
         const int k0 = kt * kTile;
         if (kt + 1 < nkv) {
             dma.load(K + hoff, Kn, k0 + kTile, N);
             dma.load(V + hoff, Vn, k0 + kTile, N);
         }
-        const bool edge = (causal && kt == tile) || q_tail || k0 + kTile > N;
         // S^T = K Q^T and dP^T = V dO^T for this wave's 32 keys x 32 queries:
         // s[nb][kb] holds keys 4g+i of key block kb for query block nb.
         f32x4 s[2][2], dp[2][2];
@@ -203,15 +231,9 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
         }
         bf16x8 tf[2], rf[2];
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
-            const int qrow = q0w + nb * 16 + c16;
-            if (edge)
-                dq_probs<true>(s[nb], dp[nb], c, lse2[nb], Di[nb], k0 + 32 * kh, g, qrow, N,
-                               causal, tf[nb], rf[nb]);
-            else
-                dq_probs<false>(s[nb], dp[nb], c, lse2[nb], Di[nb], k0 + 32 * kh, g, qrow, N,
-                                causal, tf[nb], rf[nb]);
-        }
+        for (int nb = 0; nb < 2; ++nb)
+            dq_probs<MASK>(s[nb], dp[nb], c, lse2[nb], Di[nb], k0 + 32 * kh, g,
+                           q0w + nb * 16 + c16, N, causal, tf[nb], rf[nb]);
         // A^T[d][query] += K^T[d][key] t^T[key][query] (and B^T with r); the
         // row sums rho, m come from a constant ones operand.
 #pragma unroll
@@ -233,9 +255,18 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
         __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the next tile
         __syncthreads();
     };
-    for (int kt = 0; kt < nkv; kt += 2) {
-        step(kt, KV0[0], KV0[1], KV1[0], KV1[1]);
-        if (kt + 1 < nkv) step(kt + 1, KV1[0], KV1[1], KV0[0], KV0[1]);
+    const std::false_type plain;
+    const std::true_type masked;
+    int kt = 0;
+    for (; kt + 1 < nplain; kt += 2) {
+        step(plain, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
+        step(plain, kt + 1, KV1[0], KV1[1], KV0[0], KV0[1]);
+    }
+    if (kt < nplain) {
+        step(plain, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
+        if (kt + 1 < nkv) step(masked, kt + 1, KV1[0], KV1[1], KV0[0], KV0[1]);
+    } else if (kt < nkv) {
+        step(masked, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
     }
 
     // Add the partials of the two waves that own the same queries (one query
@@ -306,46 +337,38 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
                 lam_out[soff + qrow] = lam;
             }
         }
+        // Row statistics of the key-major pass, padded to whole tiles:
+        // log2-scaled LSE (+inf beyond N) and D (0 beyond N).
+        if (g == 0) {
+            L2p[(size_t)bh * Np + qrow] = lse2[nb];
+            Dp[(size_t)bh * Np + qrow] = Di[nb];
+        }
     }
 }
 
 // ----------------------------------------------------------- key-major pass
 // P, r, t of one 16-key x 16-query block: s, dp hold queries 4g+i of the
 // block for this lane's key; they fill half `half` of the B operands tf, rf.
+// Query rows beyond N have log2-LSE = +inf (P = 0); key rows beyond N are
+// never stored; so only the causal diagonal needs a mask.
 template <bool MASK>
 __device__ __forceinline__ void dkdv_probs(const f32x4& s, const f32x4& dp, const f32x4& l2,
                                            const f32x4& dd, float c, int qb, int g, int krow,
-                                           int N, int causal, int half, bf16x8& tf, bf16x8& rf) {
+                                           int half, bf16x8& tf, bf16x8& rf) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         float P = fexp2(fmaf(s[i], c, -l2[i]));
-        if constexpr (MASK) {
-            const int query = qb + 4 * g + i;
-            const bool ok = krow < N && query < N && (!causal || krow <= query);
-            P = ok ? P : 0.f;
-        }
+        if constexpr (MASK) P = (krow <= qb + 4 * g + i) ? P : 0.f;
         tf[half * 4 + i] = to_bf16(P * (dp[i] - dd[i]));
         rf[half * 4 + i] = to_bf16(P);
     }
-}
-
-// Four consecutive FP32 row statistics starting at row `row`, rows clamped to
-// N - 1 (tail rows are masked by the caller).  One 16-byte load when the four
-// rows exist and the address is 16-byte aligned.
-__device__ __forceinline__ f32x4 ld_stat4(const float* base, int row, int N) {
-    if (row + 3 < N && (reinterpret_cast<uintptr_t>(base + row) & 15) == 0)
-        return *reinterpret_cast<const f32x4*>(base + row);
-    f32x4 v;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = base[min(row + i, N - 1)];
-    return v;
 }
 
 template <int D, bool GPROJ>
 __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dkdv_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
-    const float* __restrict__ LSE, const float* __restrict__ Drow,
+    const float* __restrict__ L2p, const float* __restrict__ Dp,
     const uint16_t* __restrict__ Z, uint16_t* __restrict__ dK, uint16_t* __restrict__ dV,
     int BH, int N, int causal, float scale) {
     constexpr int MB = D / 16;
@@ -359,26 +382,33 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     __shared__ __attribute__((aligned(16))) uint16_t T1[NT][kTile * D];
 
     const int T = (N + kTile - 1) / kTile;
+    const int Np = T * kTile;
     int bh, tile;
     map_block(blockIdx.x, BH, T, false, &bh, &tile);
     const size_t hoff = (size_t)bh * N * D;
-    const size_t soff = (size_t)bh * N;
+    const float* l2h = L2p + (size_t)bh * Np;
+    const float* ddh = Dp + (size_t)bh * Np;
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, c16 = lane & 15;
     const int kh = wave & 1;   // which 32 of the workgroup's 64 keys
     const int qh = wave >> 1;  // which 32 of each 64-query tile
     const int k0w = tile * kTile + 32 * kh;
 
     // K^T and V^T as B operands: column = this lane's key of block kb, k = d.
+    // Rows beyond N load as zero.
+    const uint32_t tbytes = (uint32_t)N * (2 * D);
+    const rsrc_t rk = make_rsrc(K + hoff, tbytes);
+    const rsrc_t rv = make_rsrc(V + hoff, tbytes);
     bf16x8 kf[2][KC], vf[2][KC];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int kc = 0; kc < KC; ++kc) {
             const int krow = k0w + kb * 16 + c16;
-            kf[kb][kc] = __builtin_bit_cast(bf16x8, ld_row16(K + hoff, krow, N, D, kc * 32 + 8 * g));
-            vf[kb][kc] = __builtin_bit_cast(bf16x8, ld_row16(V + hoff, krow, N, D, kc * 32 + 8 * g));
+            kf[kb][kc] = __builtin_bit_cast(bf16x8, ld_row16<D>(rk, krow, kc * 32 + 8 * g));
+            vf[kb][kc] = __builtin_bit_cast(bf16x8, ld_row16<D>(rv, krow, kc * 32 + 8 * g));
         }
     const float c = scale * kLog2e;
 
@@ -395,39 +425,60 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     }
 
     const int qt0 = causal ? tile : 0;
-    const bool k_tail = tile * kTile + kTile > N;
     const uint16_t* src[NT];
     src[0] = Q + hoff;
     src[1] = dO + hoff;
     if (GPROJ) src[NT - 1] = Z + hoff;
 
+    // Rows beyond N are never written by the DMA: zero both buffers once so
+    // every value a product can read is finite.
+    {
+        u32x4* z0 = reinterpret_cast<u32x4*>(&T0[0][0]);
+        u32x4* z1 = reinterpret_cast<u32x4*>(&T1[0][0]);
+        constexpr int n16 = (int)(sizeof(T0) / 16);
+#pragma unroll
+        for (int i = tid; i < n16; i += kThreads) {
+            z0[i] = u32x4{0u, 0u, 0u, 0u};
+            z1[i] = u32x4{0u, 0u, 0u, 0u};
+        }
+    }
+    __syncthreads();
+
     TileDma<D> dma;
-    dma.init(tid);
+    dma.init(lane, wave);
     auto load_tile = [&](uint16_t (*dst)[kTile * D], int q0) {
 #pragma unroll
         for (int t = 0; t < NT; ++t) dma.load(src[t], dst[t], q0, N);
     };
+    // Row statistics (log2-LSE, D) of this wave's 32 queries of a tile: four
+    // consecutive rows per lane, from the tile-padded arrays.
+    f32x4 l2[2], dd[2];
+    auto load_stats = [&](int q0, f32x4 (&l)[2], f32x4 (&d)[2]) {
+#pragma unroll
+        for (int mq = 0; mq < 2; ++mq) {
+            const int qr = q0 + 32 * qh + mq * 16 + 4 * g;
+            l[mq] = *reinterpret_cast<const f32x4*>(l2h + qr);
+            d[mq] = *reinterpret_cast<const f32x4*>(ddh + qr);
+        }
+    };
+    load_stats(qt0 * kTile, l2, dd);
     load_tile(T0, qt0 * kTile);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
-    // One query tile: compute on `cur` while the DMA fills `nxt` with the next.
-    auto step = [&](int qt, uint16_t (*cur)[kTile * D], uint16_t (*nxt)[kTile * D]) {
+    // One query tile: compute on `cur` while the DMA fills `nxt` with the next
+    // tile and the next tile's statistics arrive in registers.
+    auto step = [&](auto masked, int qt, uint16_t (*cur)[kTile * D], uint16_t (*nxt)[kTile * D]) {
+        constexpr bool MASK = decltype(masked)::value;
         const int q0 = qt * kTile;
-        // Row statistics of this wave's 32 queries, straight from global memory
-        // (issued before the DMA so the wait for them does not cover it).
-        f32x4 l2[2], dd[2];
-#pragma unroll
-        for (int mq = 0; mq < 2; ++mq) {
-            const int qr = q0 + 32 * qh + mq * 16 + 4 * g;
-            l2[mq] = ld_stat4(LSE + soff, qr, N);
-            dd[mq] = ld_stat4(Drow + soff, qr, N);
+        f32x4 l2n[2], ddn[2];
+        if (qt + 1 < T) {
+            load_stats(q0 + kTile, l2n, ddn);
+            load_tile(nxt, q0 + kTile);
         }
-        if (qt + 1 < T) load_tile(nxt, q0 + kTile);
         const uint16_t* Qc = cur[0];
         const uint16_t* Uc = cur[1];
         const uint16_t* Zc = cur[NT - 1];
-        const bool edge = (causal && qt == tile) || k_tail || q0 + kTile > N;
 
         // S = Q K^T and dP = dO V^T for this wave's 32 queries x 32 keys, one
         // 16 x 16 block at a time: s holds queries 4g+i of query block mq for
@@ -443,7 +494,6 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
                 qa[kc] = ld_b128(Qc + tile_off<D>(row, kc * 32 + 8 * g));
                 ua[kc] = ld_b128(Uc + tile_off<D>(row, kc * 32 + 8 * g));
             }
-            const f32x4 l2m = l2[mq] * kLog2e;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
                 f32x4 sv = {0.f, 0.f, 0.f, 0.f}, dpv = {0.f, 0.f, 0.f, 0.f};
@@ -452,12 +502,8 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
                     sv = mfma_16x16x32(qa[kc], kf[kb][kc], sv);
                     dpv = mfma_16x16x32(ua[kc], vf[kb][kc], dpv);
                 }
-                const int krow = k0w + kb * 16 + c16;
-                const int qb = q0 + 32 * qh + mq * 16;
-                if (edge)
-                    dkdv_probs<true>(sv, dpv, l2m, dd[mq], c, qb, g, krow, N, causal, mq, tf[kb], rf[kb]);
-                else
-                    dkdv_probs<false>(sv, dpv, l2m, dd[mq], c, qb, g, krow, N, causal, mq, tf[kb], rf[kb]);
+                dkdv_probs<MASK>(sv, dpv, l2[mq], dd[mq], c, q0 + 32 * qh + mq * 16, g,
+                                 k0w + kb * 16 + c16, mq, tf[kb], rf[kb]);
             }
         }
         // dV^T[dv][key] += dO^T r ; dK^T += Q^T t ; C^T += Z^T r.
@@ -478,10 +524,32 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
         }
         __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the next tile
         __syncthreads();
+        if (qt + 1 < T) {
+#pragma unroll
+            for (int mq = 0; mq < 2; ++mq) {
+                l2[mq] = l2n[mq];
+                dd[mq] = ddn[mq];
+            }
+        }
     };
-    for (int qt = qt0; qt < T; qt += 2) {
-        step(qt, T0, T1);
-        if (qt + 1 < T) step(qt + 1, T1, T0);
+    const std::false_type plain;
+    const std::true_type masked;
+    // Causal: only the diagonal tile (the first one) needs a mask.
+    int qt = qt0;
+    if (causal) {
+        step(masked, qt, T0, T1);
+        ++qt;
+        for (; qt + 1 < T; qt += 2) {
+            step(plain, qt, T1, T0);
+            step(plain, qt + 1, T0, T1);
+        }
+        if (qt < T) step(plain, qt, T1, T0);
+    } else {
+        for (; qt + 1 < T; qt += 2) {
+            step(plain, qt, T0, T1);
+            step(plain, qt + 1, T1, T0);
+        }
+        if (qt < T) step(plain, qt, T0, T1);
     }
 
     // Add the partials of the two waves that own the same keys (one key block
@@ -535,13 +603,14 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
 
 hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                          const uint16_t* O, const uint16_t* dO, const float* LSE, float* Drow,
-                         uint16_t* dQ, float* rho, float* msum, float* lambda, uint16_t* Z,
-                         int mode, const Shape& s, hipStream_t st) {
+                         float* L2p, float* Dp, uint16_t* dQ, float* rho, float* msum,
+                         float* lambda, uint16_t* Z, int mode, const Shape& s, hipStream_t st) {
     const int T = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
-#define GPA_DQ(DD, GP, WZ)                                                                      \
-    bwd_dq_kernel<DD, GP, WZ><<<grid, block, 0, st>>>(Q, K, V, O, dO, LSE, Drow, dQ, rho, msum, \
-                                                      lambda, Z, s.BH, s.N, s.causal, s.scale)
+#define GPA_DQ(DD, GP, WZ)                                                                   \
+    bwd_dq_kernel<DD, GP, WZ><<<grid, block, 0, st>>>(Q, K, V, O, dO, LSE, Drow, L2p, Dp, dQ, \
+                                                      rho, msum, lambda, Z, s.BH, s.N,       \
+                                                      s.causal, s.scale)
     if (s.d == 64) {
         if (mode == 2) GPA_DQ(64, true, true);
         else if (mode == 1) GPA_DQ(64, true, false);
@@ -556,14 +625,14 @@ hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V
 }
 
 hipError_t launch_bwd_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                           const uint16_t* dO, const float* LSE, const float* Drow,
+                           const uint16_t* dO, const float* L2p, const float* Dp,
                            const uint16_t* Z, uint16_t* dK, uint16_t* dV, int mode,
                            const Shape& s, hipStream_t st) {
     const int T = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
     const bool gp = mode == 2;
 #define GPA_DKDV(DD, GP)                                                             \
-    bwd_dkdv_kernel<DD, GP><<<grid, block, 0, st>>>(Q, K, V, dO, LSE, Drow, Z, dK, dV, \
+    bwd_dkdv_kernel<DD, GP><<<grid, block, 0, st>>>(Q, K, V, dO, L2p, Dp, Z, dK, dV, \
                                                     s.BH, s.N, s.causal, s.scale)
     if (s.d == 64) {
         if (gp) GPA_DKDV(64, true); else GPA_DKDV(64, false);

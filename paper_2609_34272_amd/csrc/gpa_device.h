@@ -9,6 +9,7 @@ namespace gpa {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // FP32 log2(e), rounded to FP32.
 constexpr float kLog2e = 1.44269504088896340736f;
@@ -54,44 +55,60 @@ __device__ __forceinline__ int tile_off(int r, int col) {
     return r * D + (((col >> 3) ^ swz(r)) << 3) + (col & 7);
 }
 
+// Raw buffer resource over the `bytes` bytes at `base` (stride 0, the gfx9
+// data-format word).  The hardware range-checks every buffer load against
+// `bytes`: a load at or beyond it returns zero and touches no memory, so tile
+// tails need no clamping or masking of addresses.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+
+// 16-byte buffer load at byte offset `off` (zero beyond the resource).
+__device__ __forceinline__ u32x4 buf_ld16(rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
 // Direct global -> LDS staging of one 64-row tile with the gfx950 LDS DMA load
-// (global_load_lds_dwordx4): lane L of a wave writes 16 bytes at M0 + 16 L,
-// so each wave call fills a contiguous 1 KB of the swizzled tile and every
-// lane loads the global chunk that the swizzle places in its slot.  No
-// registers or LDS write instructions are involved; completion is tracked by
-// vmcnt.  Rows at or beyond N are loaded from row N-1 instead (finite data that
-// the tail-tile masks zero out), so no load leaves the tensor.
+// (buffer_load_dwordx4 ... lds): lane L of a wave writes 16 bytes at
+// M0 + 16 L, so each wave call fills a contiguous 1 KB of the swizzled tile
+// and every lane loads the global chunk that the swizzle places in its slot.
+// No registers or LDS write instructions are involved; completion is tracked
+// by vmcnt.  The resource of a call starts at the tile's first row and ends at
+// the tensor's last row, so rows at or beyond N are range-checked away (the
+// LDS slot keeps whatever it held; callers make that harmless).
 template <int D>
 struct TileDma {
     static constexpr int CALLS = kTile * D * 2 / (kThreads * 16);
-    int row[CALLS];   // tile row of this lane's chunk in call k
-    int col[CALLS];   // logical column of that chunk
-    int lds[CALLS];   // byte offset of this wave's 1 KB block (wave-uniform)
+    uint32_t voff[CALLS];  // byte offset, inside the tile, of this lane's chunk in call k
+    uint32_t lds[CALLS];   // byte offset of this wave's 1 KB block (wave-uniform)
 
-    __device__ __forceinline__ void init(int tid) {
-        const int lane = tid & 63, wave = tid >> 6;
+    __device__ __forceinline__ void init(int lane, int wave) {
 #pragma unroll
         for (int k = 0; k < CALLS; ++k) {
             const int b = (k * 4 + wave) * 1024 + 16 * lane;
             const int r = b / (2 * D);
             const int p = (b - r * 2 * D) / 16;
-            row[k] = r;
-            col[k] = (p ^ swz(r)) * 8;
-            lds[k] = (k * 4 + wave) * 1024;
+            voff[k] = (uint32_t)(r * 2 * D + ((p ^ swz(r)) * 16));
+            lds[k] = (uint32_t)((k * 4 + wave) * 1024);
         }
     }
-    __device__ __forceinline__ void load(const uint16_t* src, uint16_t* dst, int row0,
+    // Stage rows [row0, row0 + 64) of the [N, D] tensor at `head` into `dst`.
+    __device__ __forceinline__ void load(const uint16_t* head, uint16_t* dst, int row0,
                                          int N) const {
-        const bool full = row0 + kTile <= N;
+        const rsrc_t r = make_rsrc(head + (size_t)row0 * D, (uint32_t)(N - row0) * (2 * D));
+        // The builtin exists only for the device target; without this guard the
+        // host pass silently drops the launch stubs of kernels that use it.
+#if defined(__HIP_DEVICE_COMPILE__)
 #pragma unroll
-        for (int k = 0; k < CALLS; ++k) {
-            int r = row0 + row[k];
-            if (!full) r = r < N ? r : N - 1;
-            const uint16_t* gp = src + (size_t)r * D + col[k];
-            __builtin_amdgcn_global_load_lds(
-                (const __attribute__((address_space(1))) void*)gp,
-                (__attribute__((address_space(3))) void*)((char*)dst + lds[k]), 16, 0, 0);
-        }
+        for (int k = 0; k < CALLS; ++k)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                r, (__attribute__((address_space(3))) void*)((char*)dst + lds[k]), 16, voff[k],
+                0, 0, 0);
+#else
+        (void)r;
+        (void)dst;
+#endif
     }
 };
 
@@ -132,20 +149,15 @@ __device__ __forceinline__ void st_bf16x4(uint16_t* p, float a, float b, float c
     *reinterpret_cast<bf16x4*>(p) = v;
 }
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
 // BF16 halves of a packed 32-bit word, widened exactly to FP32.
 __device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-// 16-byte global load of row `row` (clamped into [0, N)) at column `col`;
-// rows at or beyond N read as zero.  Branch-free and always in bounds.
-__device__ __forceinline__ u32x4 ld_row16(const uint16_t* base, int row, int N, int D, int col) {
-    const int r = row < N ? row : N - 1;
-    u32x4 w = *reinterpret_cast<const u32x4*>(base + (size_t)r * D + col);
-    const uint32_t keep = row < N ? 0xFFFFFFFFu : 0u;
-    w[0] &= keep; w[1] &= keep; w[2] &= keep; w[3] &= keep;
-    return w;
+// 16-byte load of row `row` at column `col` of a [N, D] tensor whose buffer
+// resource `r` covers exactly its N rows: rows at or beyond N read as zero.
+template <int D>
+__device__ __forceinline__ u32x4 ld_row16(rsrc_t r, int row, int col) {
+    return buf_ld16(r, (uint32_t)(row * D + col) * 2u);
 }
 
 // MFMA A operand whose row 0 is all ones and rows 1..15 zero: multiplying it

@@ -18,6 +18,8 @@
 #include "gpa_device.h"
 #include "gpa_launch.h"
 
+#include <type_traits>
+
 namespace gpa {
 namespace {
 
@@ -39,20 +41,21 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
     map_block(blockIdx.x, BH, T, causal != 0, &bh, &tile);
     const size_t hoff = (size_t)bh * N * D;
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, c16 = lane & 15;
     const int qh = wave & 1;   // which 32 of the workgroup's 64 queries
     const int kh = wave >> 1;  // which 32 of each 64-key tile
     const int q0w = tile * kTile + 32 * qh;
 
     // Q^T as the B operand: column = this lane's query of block nb, k = d.
+    const rsrc_t rq = make_rsrc(Q + hoff, (uint32_t)N * (2 * D));
     bf16x8 qf[2][KC];
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
         for (int kc = 0; kc < KC; ++kc)
-            qf[nb][kc] = __builtin_bit_cast(
-                bf16x8, ld_row16(Q + hoff, q0w + nb * 16 + c16, N, D, kc * 32 + 8 * g));
+            qf[nb][kc] = __builtin_bit_cast(bf16x8, ld_row16<D>(rq, q0w + nb * 16 + c16, kc * 32 + 8 * g));
 
     const float c = scale * kLog2e;  // fl32(alpha log2 e)
     float mrun[2] = {-INFINITY, -INFINITY};  // running maximum of the unscaled logits
@@ -65,15 +68,34 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
 
     const int kv_end = causal ? min(N, (tile + 1) * kTile) : N;
     const int nkv = (kv_end + kTile - 1) / kTile;
+    // Only the last key tile can need masks: the diagonal tile (causal) or the
+    // key tail (N not a multiple of the tile).
+    const int nplain = (causal || (N % kTile)) ? nkv - 1 : nkv;
+
+    // Rows beyond N are never written by the DMA: zero both buffers once so
+    // every value a product can read is finite.
+    {
+        u32x4* z0 = reinterpret_cast<u32x4*>(&KV0[0][0]);
+        u32x4* z1 = reinterpret_cast<u32x4*>(&KV1[0][0]);
+        constexpr int n16 = (int)(sizeof(KV0) / 16);
+#pragma unroll
+        for (int i = tid; i < n16; i += kThreads) {
+            z0[i] = u32x4{0u, 0u, 0u, 0u};
+            z1[i] = u32x4{0u, 0u, 0u, 0u};
+        }
+    }
+    __syncthreads();
 
     TileDma<D> dma;
-    dma.init(tid);
+    dma.init(lane, wave);
     dma.load(K + hoff, KV0[0], 0, N);
     dma.load(V + hoff, KV0[1], 0, N);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
-    auto step = [&](int kt, const uint16_t* Kc, const uint16_t* Vc, uint16_t* Kn, uint16_t* Vn) {
+    auto step = [&](auto masked, int kt, const uint16_t* Kc, const uint16_t* Vc, uint16_t* Kn,
+                    uint16_t* Vn) {
+        constexpr bool MASK = decltype(masked)::value;
         const int k0 = kt * kTile;
         if (kt + 1 < nkv) {
             dma.load(K + hoff, Kn, k0 + kTile, N);
@@ -93,8 +115,7 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
                 for (int nb = 0; nb < 2; ++nb) s[nb][kb] = mfma_16x16x32(ka, qf[nb][kc], s[nb][kb]);
             }
         }
-        // Only the diagonal tile and the key tail need masks (uniform branch).
-        if ((causal && kt == tile) || k0 + kTile > N) {
+        if constexpr (MASK) {
 #pragma unroll
             for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
@@ -145,9 +166,18 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
         __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the next tile
         __syncthreads();
     };
-    for (int kt = 0; kt < nkv; kt += 2) {
-        step(kt, KV0[0], KV0[1], KV1[0], KV1[1]);
-        if (kt + 1 < nkv) step(kt + 1, KV1[0], KV1[1], KV0[0], KV0[1]);
+    const std::false_type plain;
+    const std::true_type masked;
+    int kt = 0;
+    for (; kt + 1 < nplain; kt += 2) {
+        step(plain, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
+        step(plain, kt + 1, KV1[0], KV1[1], KV0[0], KV0[1]);
+    }
+    if (kt < nplain) {
+        step(plain, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
+        if (kt + 1 < nkv) step(masked, kt + 1, KV1[0], KV1[1], KV0[0], KV0[1]);
+    } else if (kt < nkv) {
+        step(masked, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
     }
 
     // Merge the two key halves of each query (waves w and w + 2): waves 2, 3
