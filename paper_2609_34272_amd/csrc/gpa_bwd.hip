@@ -207,8 +207,15 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
             dma.load(K + hoff, Kn, k0 + kTile, N);
             dma.load(V + hoff, Vn, k0 + kTile, N);
         }
+        // Keep the loads of the next tile at the top of the step: left alone,
+        // the scheduler sinks them next to the closing wait, which exposes
+        // their whole latency.
+        __builtin_amdgcn_sched_barrier(0);
         // S^T = K Q^T and dP^T = V dO^T for this wave's 32 keys x 32 queries:
         // s[nb][kb] holds keys 4g+i of key block kb for query block nb.
+        // Raise this wave's issue priority while it feeds the matrix core, so
+        // that the other wave on the SIMD fills the vector ALU meanwhile.
+        __builtin_amdgcn_s_setprio(1);
         f32x4 s[2][2], dp[2][2];
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
@@ -236,6 +243,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
                            q0w + nb * 16 + c16, N, causal, tf[nb], rf[nb]);
         // A^T[d][query] += K^T[d][key] t^T[key][query] (and B^T with r); the
         // row sums rho, m come from a constant ones operand.
+        __builtin_amdgcn_s_setprio(0);
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
             const bf16x8 ka = ld_tr_operand<D>(Kc, 32 * kh, mb * 16, c16, g);
@@ -476,6 +484,10 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
             load_stats(q0 + kTile, l2n, ddn);
             load_tile(nxt, q0 + kTile);
         }
+        // Keep the loads of the next tile at the top of the step: left alone,
+        // the scheduler sinks them next to the closing wait, which exposes
+        // their whole latency.
+        __builtin_amdgcn_sched_barrier(0);
         const uint16_t* Qc = cur[0];
         const uint16_t* Uc = cur[1];
         const uint16_t* Zc = cur[NT - 1];
@@ -485,6 +497,9 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
         // key block kb, and P, r, t of that block go straight into half mq of
         // the key block's B operands tf[kb], rf[kb].
         bf16x8 tf[2], rf[2];
+        // Raise this wave's issue priority while it feeds the matrix core, so
+        // that the other wave on the SIMD fills the vector ALU meanwhile.
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int mq = 0; mq < 2; ++mq) {
             const int row = 32 * qh + mq * 16 + c16;
@@ -507,6 +522,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
             }
         }
         // dV^T[dv][key] += dO^T r ; dK^T += Q^T t ; C^T += Z^T r.
+        __builtin_amdgcn_s_setprio(0);
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
             const bf16x8 ua = ld_tr_operand<D>(Uc, 32 * qh, mb * 16, c16, g);

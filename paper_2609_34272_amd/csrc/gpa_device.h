@@ -77,20 +77,21 @@ __device__ __forceinline__ u32x4 buf_ld16(rsrc_t r, uint32_t off) {
 // by vmcnt.  The resource of a call starts at the tile's first row and ends at
 // the tensor's last row, so rows at or beyond N are range-checked away (the
 // LDS slot keeps whatever it held; callers make that harmless).
-template <int D>
+template <int D, int NTHR = kThreads>
 struct TileDma {
-    static constexpr int CALLS = kTile * D * 2 / (kThreads * 16);
+    static constexpr int NWAVES = NTHR / 64;
+    static constexpr int CALLS = kTile * D * 2 / (NTHR * 16);
     uint32_t voff[CALLS];  // byte offset, inside the tile, of this lane's chunk in call k
     uint32_t lds[CALLS];   // byte offset of this wave's 1 KB block (wave-uniform)
 
     __device__ __forceinline__ void init(int lane, int wave) {
 #pragma unroll
         for (int k = 0; k < CALLS; ++k) {
-            const int b = (k * 4 + wave) * 1024 + 16 * lane;
+            const int b = (k * NWAVES + wave) * 1024 + 16 * lane;
             const int r = b / (2 * D);
             const int p = (b - r * 2 * D) / 16;
             voff[k] = (uint32_t)(r * 2 * D + ((p ^ swz(r)) * 16));
-            lds[k] = (uint32_t)((k * 4 + wave) * 1024);
+            lds[k] = (uint32_t)((k * NWAVES + wave) * 1024);
         }
     }
     // Stage rows [row0, row0 + 64) of the [N, D] tensor at `head` into `dst`.
@@ -170,16 +171,29 @@ __device__ __forceinline__ bf16x8 ones_row0(int c16) {
     return a;
 }
 
+// Reductions over the four 16-lane rows of a wave (lanes c16, c16 + 16,
+// c16 + 32, c16 + 48), with the gfx950 lane-swap instructions instead of an
+// LDS round trip.  v_permlane16_swap on two copies of v leaves rows (0, 0, 2, 2)
+// in one copy and (1, 1, 3, 3) in the other; v_permlane32_swap leaves the low
+// and the high half.  Combining the two copies therefore gives every lane the
+// pairwise result (x ^ 16, then x ^ 32), bitwise the same in both partners
+// because max and + are commutative.
 __device__ __forceinline__ float xor_max(float v) {
-    v = fmaxf(v, __shfl_xor(v, 16));
-    v = fmaxf(v, __shfl_xor(v, 32));
-    return v;
+    const uint32_t u = __float_as_uint(v);
+    const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const uint32_t w = __float_as_uint(v);
+    const auto b = __builtin_amdgcn_permlane32_swap(w, w, false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
 __device__ __forceinline__ float xor_sum(float v) {
-    v += __shfl_xor(v, 16);
-    v += __shfl_xor(v, 32);
-    return v;
+    const uint32_t u = __float_as_uint(v);
+    const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const uint32_t w = __float_as_uint(v);
+    const auto b = __builtin_amdgcn_permlane32_swap(w, w, false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 // Workgroup -> (batch*head, tile).  Workgroups are dispatched round-robin over

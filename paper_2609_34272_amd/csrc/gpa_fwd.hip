@@ -101,6 +101,10 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
             dma.load(K + hoff, Kn, k0 + kTile, N);
             dma.load(V + hoff, Vn, k0 + kTile, N);
         }
+        // Keep the loads of the next tile at the top of the step: left alone,
+        // the scheduler sinks them next to the closing wait, which exposes
+        // their whole latency.
+        __builtin_amdgcn_sched_barrier(0);
         // S^T[key][query] for this wave's 32 keys x 32 queries; s[nb][kb]
         // holds keys 4g+i of key block kb for query block nb.
         f32x4 s[2][2];
