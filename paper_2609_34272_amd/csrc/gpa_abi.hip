@@ -109,25 +109,24 @@ gpa_status launched(hipError_t e, const char* what) {
 }
 
 struct BwdLayout {
-    size_t D, rho, m, lam, l2p, dp, z, total;
+    size_t D, rho, m, lam, ts, z, total;
 };
 
-// Four FP32 [B,H,N] row statistics; two FP32 [B*H, Np] copies of log2-scaled
-// LSE and D padded to whole 64-row tiles (Np = N rounded up to 64) that the
-// key-major pass reads without bounds checks; then (gproj mode only) the BF16
-// [B,H,N,d] tensor z = BF16(lambda q) that the key correction contracts.
+// Four FP32 [B,H,N] row statistics; per 64-row query tile a 512-byte block of
+// log2-scaled LSE and D (FP32 [B*H, T, 2, 64], T = N rounded up to 64, over 64)
+// that the key-major pass stages with the tile; then (gproj mode only) the
+// BF16 [B,H,N,d] tensor z = BF16(lambda q) that the key correction contracts.
 BwdLayout bwd_layout(int64_t B, int64_t H, int64_t N, int64_t d, int mode) {
     const size_t row = round_up((size_t)B * H * N * sizeof(float));
-    const size_t Np = (size_t)(N + 63) / 64 * 64;
-    const size_t padded = round_up((size_t)B * H * Np * sizeof(float));
+    const size_t T = (size_t)(N + 63) / 64;
+    const size_t tstats = round_up((size_t)B * H * T * 128 * sizeof(float));
     BwdLayout L;
     L.D = 0;
     L.rho = row;
     L.m = 2 * row;
     L.lam = 3 * row;
-    L.l2p = 4 * row;
-    L.dp = L.l2p + padded;
-    L.z = L.dp + padded;
+    L.ts = 4 * row;
+    L.z = L.ts + tstats;
     L.total = L.z + (mode == 2 ? round_up((size_t)B * H * N * d * 2) : 0);
     return L;
 }
@@ -213,21 +212,20 @@ gpa_status gpa_attn_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
     float* rho = (float*)(ws + L.rho);
     float* msum = (float*)(ws + L.m);
     float* lam = (float*)(ws + L.lam);
-    float* l2p = (float*)(ws + L.l2p);
-    float* dp = (float*)(ws + L.dp);
+    float* tstats = (float*)(ws + L.ts);
     uint16_t* zbuf = mode == 2 ? (uint16_t*)(ws + L.z) : nullptr;
 
     s = launched(timed(gpa::kKBwdDq, st,
                        [&] {
-                           return gpa::launch_bwd_dq(Q, K, V, O, dO, LSE, Drow, l2p, dp, dQ, rho,
-                                                     msum, lam, zbuf, mode, sh, st);
+                           return gpa::launch_bwd_dq(Q, K, V, O, dO, LSE, Drow, tstats, dQ, rho, msum,
+                                                     lam, zbuf, mode, sh, st);
                        }),
                  "bwd_dq");
     if (s != GPA_OK) return s;
     return launched(timed(gpa::kKBwdDkdv, st,
                           [&] {
-                              return gpa::launch_bwd_dkdv(Q, K, V, dO, l2p, dp, zbuf, dK, dV,
-                                                          mode, sh, st);
+                              return gpa::launch_bwd_dkdv(Q, K, V, dO, tstats, zbuf, dK, dV, mode,
+                                                          sh, st);
                           }),
                     "bwd_dkdv");
 }

@@ -99,7 +99,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, const uint16_t* __restrict__ O,
     const uint16_t* __restrict__ dO, const float* __restrict__ LSE, float* __restrict__ D_out,
-    float* __restrict__ L2p, float* __restrict__ Dp, uint16_t* __restrict__ dQ,
+    float* __restrict__ TS, uint16_t* __restrict__ dQ,
     float* __restrict__ rho_out, float* __restrict__ m_out, float* __restrict__ lam_out,
     uint16_t* __restrict__ Zout, int BH, int N, int causal, float scale) {
     constexpr int MB = D / 16;  // 16-column blocks of d
@@ -113,7 +113,6 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     __shared__ __attribute__((aligned(16))) uint16_t KV1[2][kTile * D];  // [K, V], buffer 1
 
     const int T = (N + kTile - 1) / kTile;
-    const int Np = T * kTile;
     int bh, tile;
     map_block(blockIdx.x, BH, T, causal != 0, &bh, &tile);
     const size_t hoff = (size_t)bh * N * D;
@@ -345,11 +344,12 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
                 lam_out[soff + qrow] = lam;
             }
         }
-        // Row statistics of the key-major pass, padded to whole tiles:
-        // log2-scaled LSE (+inf beyond N) and D (0 beyond N).
+        // The tile's statistics block for the key-major pass: log2-scaled LSE
+        // (+inf beyond N), then D (0 beyond N).
         if (g == 0) {
-            L2p[(size_t)bh * Np + qrow] = lse2[nb];
-            Dp[(size_t)bh * Np + qrow] = Di[nb];
+            float* ts = TS + ((size_t)bh * T + tile) * kStatFloats;
+            ts[qrow - tile * kTile] = lse2[nb];
+            ts[kTile + qrow - tile * kTile] = Di[nb];
         }
     }
 }
@@ -376,26 +376,30 @@ template <int D, bool GPROJ>
 __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dkdv_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
-    const float* __restrict__ L2p, const float* __restrict__ Dp,
-    const uint16_t* __restrict__ Z, uint16_t* __restrict__ dK, uint16_t* __restrict__ dV,
-    int BH, int N, int causal, float scale) {
+    const float* __restrict__ TS, const uint16_t* __restrict__ Z, uint16_t* __restrict__ dK,
+    uint16_t* __restrict__ dV, int BH, int N, int causal, float scale) {
     constexpr int MB = D / 16;
     constexpr int KC = D / 32;
     constexpr int NT = GPROJ ? 3 : 2;  // staged tensors: Q, dO (and Z = BF16(lambda Q))
     constexpr int NV = GPROJ ? 3 : 2;  // accumulators per output element: dV, dK^acc (, C)
     constexpr int PER_KB = NV * MB * 4;
-    // Query tiles, double-buffered in two separate LDS objects so the compiler
-    // can tell the tile being read from the one the DMA is filling.
-    __shared__ __attribute__((aligned(16))) uint16_t T0[NT][kTile * D];
-    __shared__ __attribute__((aligned(16))) uint16_t T1[NT][kTile * D];
+    // One ring slot: the NT query-tile tensors, then per wave the row
+    // statistics of its 32 queries (32 log2-LSE, 32 D as FP32).  Three slots in
+    // three separate LDS objects (so the compiler can tell the slot being read
+    // from those the DMA is filling): while tile i is computed on, tiles i+1
+    // and i+2 are in flight, which gives every load two steps to land.
+    constexpr int TILE_E = kTile * D;  // BF16 elements of one staged tensor
+    constexpr int STAT_E = kWaves * 128;  // 4 x 256 bytes of statistics
+    constexpr int SLOT_E = NT * TILE_E + STAT_E;
+    __shared__ __attribute__((aligned(16))) uint16_t B0[SLOT_E];
+    __shared__ __attribute__((aligned(16))) uint16_t B1[SLOT_E];
+    __shared__ __attribute__((aligned(16))) uint16_t B2[SLOT_E];
 
     const int T = (N + kTile - 1) / kTile;
-    const int Np = T * kTile;
     int bh, tile;
     map_block(blockIdx.x, BH, T, false, &bh, &tile);
     const size_t hoff = (size_t)bh * N * D;
-    const float* l2h = L2p + (size_t)bh * Np;
-    const float* ddh = Dp + (size_t)bh * Np;
+    const float* tsh = TS + (size_t)bh * T * kStatFloats;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -438,59 +442,49 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     src[1] = dO + hoff;
     if (GPROJ) src[NT - 1] = Z + hoff;
 
-    // Rows beyond N are never written by the DMA: zero both buffers once so
-    // every value a product can read is finite.
-    {
-        u32x4* z0 = reinterpret_cast<u32x4*>(&T0[0][0]);
-        u32x4* z1 = reinterpret_cast<u32x4*>(&T1[0][0]);
-        constexpr int n16 = (int)(sizeof(T0) / 16);
-#pragma unroll
-        for (int i = tid; i < n16; i += kThreads) {
-            z0[i] = u32x4{0u, 0u, 0u, 0u};
-            z1[i] = u32x4{0u, 0u, 0u, 0u};
-        }
-    }
-    __syncthreads();
-
     TileDma<D> dma;
     dma.init(lane, wave);
-    auto load_tile = [&](uint16_t (*dst)[kTile * D], int q0) {
+    // Vector-memory instructions one slot fill issues per wave: NT tensors of
+    // TileDma::CALLS each, plus one for the statistics.  Every step issues one
+    // fill (a zero fill past the last tile), so the count between a fill and
+    // the wait for it is always FILL_VM.  Rows beyond N arrive as zeros.
+    constexpr int FILL_VM = NT * TileDma<D>::CALLS + 1;
+    auto fill = [&](uint16_t* slot, int qt) {
+        const bool valid = qt < T;
 #pragma unroll
-        for (int t = 0; t < NT; ++t) dma.load(src[t], dst[t], q0, N);
+        for (int t = 0; t < NT; ++t) dma.load(src[t], slot + t * TILE_E, qt * kTile, N, valid);
+        stat_dma(tsh + (size_t)(valid ? qt : 0) * kStatFloats,
+                 reinterpret_cast<float*>(slot + NT * TILE_E) + 64 * wave, lane, qh, valid);
     };
-    // Row statistics (log2-LSE, D) of this wave's 32 queries of a tile: four
-    // consecutive rows per lane, from the tile-padded arrays.
-    f32x4 l2[2], dd[2];
-    auto load_stats = [&](int q0, f32x4 (&l)[2], f32x4 (&d)[2]) {
-#pragma unroll
-        for (int mq = 0; mq < 2; ++mq) {
-            const int qr = q0 + 32 * qh + mq * 16 + 4 * g;
-            l[mq] = *reinterpret_cast<const f32x4*>(l2h + qr);
-            d[mq] = *reinterpret_cast<const f32x4*>(ddh + qr);
-        }
-    };
-    load_stats(qt0 * kTile, l2, dd);
-    load_tile(T0, qt0 * kTile);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+    // The register operands above must have arrived before the first fill: the
+    // compiler cannot count the fills, so it must have nothing left to wait
+    // for inside the loop.
+    wait_vm_lgkm0<0>();
+    fill(B0, qt0);
+    fill(B1, qt0 + 1);
+    wait_vm_lgkm0<FILL_VM>();
+    __builtin_amdgcn_s_barrier();
 
-    // One query tile: compute on `cur` while the DMA fills `nxt` with the next
-    // tile and the next tile's statistics arrive in registers.
-    auto step = [&](auto masked, int qt, uint16_t (*cur)[kTile * D], uint16_t (*nxt)[kTile * D]) {
+    // One query tile: compute on slot `cur` while slot `nxt2` receives tile
+    // qt + 2; at the end, tile qt + 1 has landed and every wave is done with
+    // `cur`, which the next step refills.
+    auto step = [&](auto masked, int qt, const uint16_t* cur, uint16_t* nxt2) {
         constexpr bool MASK = decltype(masked)::value;
         const int q0 = qt * kTile;
-        f32x4 l2n[2], ddn[2];
-        if (qt + 1 < T) {
-            load_stats(q0 + kTile, l2n, ddn);
-            load_tile(nxt, q0 + kTile);
-        }
-        // Keep the loads of the next tile at the top of the step: left alone,
-        // the scheduler sinks them next to the closing wait, which exposes
-        // their whole latency.
+        fill(nxt2, qt + 2);
+        // Keep the loads at the top of the step: left alone, the scheduler
+        // sinks them towards the closing wait.
         __builtin_amdgcn_sched_barrier(0);
-        const uint16_t* Qc = cur[0];
-        const uint16_t* Uc = cur[1];
-        const uint16_t* Zc = cur[NT - 1];
+        const uint16_t* Qc = cur;
+        const uint16_t* Uc = cur + TILE_E;
+        const uint16_t* Zc = cur + (NT - 1) * TILE_E;
+        const float* st = reinterpret_cast<const float*>(cur + NT * TILE_E) + 64 * wave;
+        f32x4 l2[2], dd[2];
+#pragma unroll
+        for (int mq = 0; mq < 2; ++mq) {
+            l2[mq] = *reinterpret_cast<const f32x4*>(st + mq * 16 + 4 * g);
+            dd[mq] = *reinterpret_cast<const f32x4*>(st + 32 + mq * 16 + 4 * g);
+        }
 
         // S = Q K^T and dP = dO V^T for this wave's 32 queries x 32 keys, one
         // 16 x 16 block at a time: s holds queries 4g+i of query block mq for
@@ -538,35 +532,27 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
                 for (int kb = 0; kb < 2; ++kb) accC[kb][mb] = mfma_16x16x32(za, rf[kb], accC[kb][mb]);
             }
         }
-        __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the next tile
-        __syncthreads();
-        if (qt + 1 < T) {
-#pragma unroll
-            for (int mq = 0; mq < 2; ++mq) {
-                l2[mq] = l2n[mq];
-                dd[mq] = ddn[mq];
-            }
-        }
+        // Tile qt + 1 must have landed; tile qt + 2 may stay in flight.
+        wait_vm_lgkm0<FILL_VM>();
+        __builtin_amdgcn_s_barrier();
     };
     const std::false_type plain;
     const std::true_type masked;
-    // Causal: only the diagonal tile (the first one) needs a mask.
-    int qt = qt0;
-    if (causal) {
-        step(masked, qt, T0, T1);
-        ++qt;
-        for (; qt + 1 < T; qt += 2) {
-            step(plain, qt, T1, T0);
-            step(plain, qt + 1, T0, T1);
-        }
-        if (qt < T) step(plain, qt, T1, T0);
-    } else {
-        for (; qt + 1 < T; qt += 2) {
-            step(plain, qt, T0, T1);
-            step(plain, qt + 1, T1, T0);
-        }
-        if (qt < T) step(plain, qt, T0, T1);
+    // Tile t lives in slot (t - qt0) mod 3.  Causal: only the diagonal tile
+    // (the first one) needs a mask.
+    if (causal)
+        step(masked, qt0, B0, B2);
+    else
+        step(plain, qt0, B0, B2);
+    for (int qt = qt0 + 1; qt < T; qt += 3) {
+        step(plain, qt, B1, B0);
+        if (qt + 1 < T) step(plain, qt + 1, B2, B1);
+        if (qt + 2 < T) step(plain, qt + 2, B0, B2);
     }
+    // The zero fills issued by the last steps must land before B0 is reused
+    // for the reduction.
+    wait_vm_lgkm0<0>();
+    __builtin_amdgcn_s_barrier();
 
     // Add the partials of the two waves that own the same keys (one key block
     // at a time, to bound the LDS the exchange needs).
@@ -583,8 +569,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
                 if (GPROJ) red[kb][j + NV - 1] = accC[kb][mb][i];
             }
         if (kb) __syncthreads();  // the previous exchange has been read
-        pair_reduce<PER_KB, sizeof(T0) / 4>(red[kb], reinterpret_cast<float*>(&T0[0][0]), wave,
-                                             lane);
+        pair_reduce<PER_KB, sizeof(B0) / 4>(red[kb], reinterpret_cast<float*>(B0), wave, lane);
     }
     if (wave >= 2) return;
 
@@ -619,14 +604,14 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
 
 hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                          const uint16_t* O, const uint16_t* dO, const float* LSE, float* Drow,
-                         float* L2p, float* Dp, uint16_t* dQ, float* rho, float* msum,
-                         float* lambda, uint16_t* Z, int mode, const Shape& s, hipStream_t st) {
+                         float* TS, uint16_t* dQ, float* rho, float* msum, float* lambda,
+                         uint16_t* Z, int mode, const Shape& s, hipStream_t st) {
     const int T = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
 #define GPA_DQ(DD, GP, WZ)                                                                   \
-    bwd_dq_kernel<DD, GP, WZ><<<grid, block, 0, st>>>(Q, K, V, O, dO, LSE, Drow, L2p, Dp, dQ, \
-                                                      rho, msum, lambda, Z, s.BH, s.N,       \
-                                                      s.causal, s.scale)
+    bwd_dq_kernel<DD, GP, WZ><<<grid, block, 0, st>>>(Q, K, V, O, dO, LSE, Drow, TS, dQ, rho, \
+                                                      msum, lambda, Z, s.BH, s.N, s.causal,  \
+                                                      s.scale)
     if (s.d == 64) {
         if (mode == 2) GPA_DQ(64, true, true);
         else if (mode == 1) GPA_DQ(64, true, false);
@@ -641,15 +626,15 @@ hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V
 }
 
 hipError_t launch_bwd_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                           const uint16_t* dO, const float* L2p, const float* Dp,
-                           const uint16_t* Z, uint16_t* dK, uint16_t* dV, int mode,
-                           const Shape& s, hipStream_t st) {
+                           const uint16_t* dO, const float* TS, const uint16_t* Z,
+                           uint16_t* dK, uint16_t* dV, int mode, const Shape& s,
+                           hipStream_t st) {
     const int T = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
     const bool gp = mode == 2;
 #define GPA_DKDV(DD, GP)                                                             \
-    bwd_dkdv_kernel<DD, GP><<<grid, block, 0, st>>>(Q, K, V, dO, L2p, Dp, Z, dK, dV, \
-                                                    s.BH, s.N, s.causal, s.scale)
+    bwd_dkdv_kernel<DD, GP><<<grid, block, 0, st>>>(Q, K, V, dO, TS, Z, dK, dV, s.BH, s.N, \
+                                                    s.causal, s.scale)
     if (s.d == 64) {
         if (gp) GPA_DKDV(64, true); else GPA_DKDV(64, false);
     } else {

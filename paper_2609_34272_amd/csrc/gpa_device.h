@@ -69,6 +69,48 @@ __device__ __forceinline__ u32x4 buf_ld16(rsrc_t r, uint32_t off) {
     return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
 
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+
+// The same raw buffer resource as four words, for inline assembly.
+__device__ __forceinline__ i32x4 buf_desc(const void* base, uint32_t bytes) {
+    const uint64_t a = (uint64_t)(uintptr_t)base;
+    return i32x4{(int32_t)(uint32_t)a, (int32_t)((uint32_t)(a >> 32) & 0xFFFFu), (int32_t)bytes,
+                 0x00020000};
+}
+
+// 32-bit LDS address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)((__attribute__((address_space(3))) const char*)p);
+}
+
+// LDS DMA buffer loads (lane L writes 16 or 4 bytes at M0 + 16 L or M0 + 4 L;
+// lanes out of the resource's range write zeros).  They are issued as inline
+// assembly so that the compiler's wait-count insertion does not see them: its
+// alias tracking of LDS DMA targets is imprecise and would wait for every
+// outstanding tile load before each LDS read.  The kernels therefore order
+// these loads themselves, with explicit vmcnt waits and barriers.  The s_nop
+// covers the M0-write to LDS-DMA hazard.
+__device__ __forceinline__ void lds_dma16(i32x4 desc, uint32_t m0, uint32_t voff) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :
+                 : "s"(m0), "v"(voff), "s"(desc)
+                 : "memory");
+#else
+    (void)desc; (void)m0; (void)voff;
+#endif
+}
+__device__ __forceinline__ void lds_dma4(i32x4 desc, uint32_t m0, uint32_t voff) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+                 :
+                 : "s"(m0), "v"(voff), "s"(desc)
+                 : "memory");
+#else
+    (void)desc; (void)m0; (void)voff;
+#endif
+}
+
 // Direct global -> LDS staging of one 64-row tile with the gfx950 LDS DMA load
 // (buffer_load_dwordx4 ... lds): lane L of a wave writes 16 bytes at
 // M0 + 16 L, so each wave call fills a contiguous 1 KB of the swizzled tile
@@ -95,23 +137,43 @@ struct TileDma {
         }
     }
     // Stage rows [row0, row0 + 64) of the [N, D] tensor at `head` into `dst`.
-    __device__ __forceinline__ void load(const uint16_t* head, uint16_t* dst, int row0,
-                                         int N) const {
-        const rsrc_t r = make_rsrc(head + (size_t)row0 * D, (uint32_t)(N - row0) * (2 * D));
-        // The builtin exists only for the device target; without this guard the
-        // host pass silently drops the launch stubs of kernels that use it.
-#if defined(__HIP_DEVICE_COMPILE__)
+    // With valid == false nothing is read and the slot is filled with zeros
+    // (every lane is then out of range), which keeps the number of
+    // vector-memory instructions per step fixed.
+    __device__ __forceinline__ void load(const uint16_t* head, uint16_t* dst, int row0, int N,
+                                         bool valid = true) const {
+        const int r0 = valid ? row0 : 0;
+        const i32x4 desc =
+            buf_desc(head + (size_t)r0 * D, valid ? (uint32_t)(N - r0) * (2 * D) : 0u);
+        const uint32_t base = lds_addr(dst);
 #pragma unroll
-        for (int k = 0; k < CALLS; ++k)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                r, (__attribute__((address_space(3))) void*)((char*)dst + lds[k]), 16, voff[k],
-                0, 0, 0);
-#else
-        (void)r;
-        (void)dst;
-#endif
+        for (int k = 0; k < CALLS; ++k) lds_dma16(desc, base + lds[k], voff[k]);
     }
 };
+
+// Per query tile, the key-major pass reads the tile's row statistics from a
+// 512-byte block: 64 log2-scaled LSE values, then 64 values of D (FP32).
+constexpr int kStatFloats = 2 * kTile;
+
+// LDS DMA of the statistics one wave needs: its 32 query rows (half `qh` of
+// the tile) of log2-LSE and of D, 4 bytes per lane, into the 256 bytes at
+// `dst` ([32 log2-LSE][32 D]).  A 4-byte LDS DMA writes lane L at M0 + 4 L, so
+// the wave's footprint is exactly those 256 bytes.  valid == false writes
+// zeros and reads nothing.
+__device__ __forceinline__ void stat_dma(const float* tile_stats, float* dst, int lane, int qh,
+                                         bool valid) {
+    const i32x4 desc = buf_desc(tile_stats, valid ? kStatFloats * 4 : 0);
+    const uint32_t row = (uint32_t)(32 * qh + (lane & 31)) + (lane < 32 ? 0u : (uint32_t)kTile);
+    lds_dma4(desc, lds_addr(dst), row * 4u);
+}
+
+// s_waitcnt with vmcnt <= VM (gfx9 encoding: vmcnt[3:0] | expcnt[6:4] |
+// lgkmcnt[11:8] | vmcnt[5:4] at bits 15:14), lgkmcnt = 0, expcnt untouched.
+template <int VM>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+    static_assert(VM >= 0 && VM < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((VM & 15) | (7 << 4) | ((VM >> 4) << 14));
+}
 
 // Transposed MFMA operand read straight from a row-major LDS tile X[k][n]
 // with the gfx950 LDS transpose load ds_read_b64_tr_b16.  Within each 16-lane

@@ -32,18 +32,19 @@ hipError_t launch_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, u
 
 // Query-major pass: writes D = rowsum(dO * O) and dQ; in the gproj modes also
 // rho, m, lambda (zero in plain mode); in gproj mode also Z = BF16(lambda Q)
-// ([BH, N, d], BF16).  L2p and Dp ([BH, Np], Np = N rounded up to the tile)
-// receive LSE * log2(e) (+inf beyond N) and D (0 beyond N) for the key pass.
+// ([BH, N, d], BF16).  TS ([BH, T, 2, 64] FP32, T = tiles of 64 rows)
+// receives per tile LSE * log2(e) (+inf beyond N) and D (0 beyond N) for the
+// key pass.
 hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                          const uint16_t* O, const uint16_t* dO, const float* LSE, float* Drow,
-                         float* L2p, float* Dp, uint16_t* dQ, float* rho, float* msum,
-                         float* lambda, uint16_t* Z, int mode, const Shape& s, hipStream_t st);
+                         float* TS, uint16_t* dQ, float* rho, float* msum, float* lambda,
+                         uint16_t* Z, int mode, const Shape& s, hipStream_t st);
 
 // Key-major pass: dV = r^T dO, dK = t^T Q (minus r^T Z in gproj mode).
 hipError_t launch_bwd_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                           const uint16_t* dO, const float* L2p, const float* Dp,
-                           const uint16_t* Z, uint16_t* dK, uint16_t* dV, int mode,
-                           const Shape& s, hipStream_t st);
+                           const uint16_t* dO, const float* TS, const uint16_t* Z,
+                           uint16_t* dK, uint16_t* dV, int mode, const Shape& s,
+                           hipStream_t st);
 
 // FP32 baseline.
 hipError_t launch_f32_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, float* O32,
