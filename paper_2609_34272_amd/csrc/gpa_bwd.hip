@@ -449,12 +449,22 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     // fill (a zero fill past the last tile), so the count between a fill and
     // the wait for it is always FILL_VM.  Rows beyond N arrive as zeros.
     constexpr int FILL_VM = NT * TileDma<D>::CALLS + 1;
-    auto fill = [&](uint16_t* slot, int qt) {
+    // Piece j (0 <= j < FILL_VM) of a fill: the statistics first, then the
+    // tensors' calls in order.  A step spreads its fill's pieces over its
+    // compute so the loads do not all queue at once.
+    auto fill_piece = [&](uint16_t* slot, int qt, int j) {
         const bool valid = qt < T;
+        if (j == 0) {
+            stat_dma(tsh + (size_t)(valid ? qt : 0) * kStatFloats,
+                     reinterpret_cast<float*>(slot + NT * TILE_E) + 64 * wave, lane, qh, valid);
+        } else if (j < FILL_VM) {
+            const int t = (j - 1) / TileDma<D>::CALLS, k = (j - 1) % TileDma<D>::CALLS;
+            dma.load_call(src[t], slot + t * TILE_E, qt * kTile, N, valid, k);
+        }
+    };
+    auto fill = [&](uint16_t* slot, int qt) {
 #pragma unroll
-        for (int t = 0; t < NT; ++t) dma.load(src[t], slot + t * TILE_E, qt * kTile, N, valid);
-        stat_dma(tsh + (size_t)(valid ? qt : 0) * kStatFloats,
-                 reinterpret_cast<float*>(slot + NT * TILE_E) + 64 * wave, lane, qh, valid);
+        for (int j = 0; j < FILL_VM; ++j) fill_piece(slot, qt, j);
     };
     // The register operands above must have arrived before the first fill: the
     // compiler cannot count the fills, so it must have nothing left to wait
@@ -471,10 +481,12 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     auto step = [&](auto masked, int qt, const uint16_t* cur, uint16_t* nxt2) {
         constexpr bool MASK = decltype(masked)::value;
         const int q0 = qt * kTile;
-        fill(nxt2, qt + 2);
-        // Keep the loads at the top of the step: left alone, the scheduler
-        // sinks them towards the closing wait.
-        __builtin_amdgcn_sched_barrier(0);
+        // The fill of tile qt + 2 is issued in pieces through the step (a few
+        // first, one after each S/dP block, the rest in the dV/dK phase); it
+        // has until the end of step qt + 1 to land.
+        constexpr int AT_START = FILL_VM > 6 ? FILL_VM - 6 : 1;
+#pragma unroll
+        for (int j = 0; j < AT_START; ++j) fill_piece(nxt2, qt + 2, j);
         const uint16_t* Qc = cur;
         const uint16_t* Uc = cur + TILE_E;
         const uint16_t* Zc = cur + (NT - 1) * TILE_E;
@@ -485,6 +497,18 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
             l2[mq] = *reinterpret_cast<const f32x4*>(st + mq * 16 + 4 * g);
             dd[mq] = *reinterpret_cast<const f32x4*>(st + 32 + mq * 16 + 4 * g);
         }
+        // The transposed A operands of the first two column blocks of the
+        // dV/dK/C products are read now, so their LDS latency hides behind the
+        // S/dP products and the exponentials.
+        bf16x8 opd[2][NT];
+        auto read_ops = [&](bf16x8 (&o)[NT], int mb) {
+            o[0] = ld_tr_operand<D>(Uc, 32 * qh, mb * 16, c16, g);
+            o[1] = ld_tr_operand<D>(Qc, 32 * qh, mb * 16, c16, g);
+            if (GPROJ) o[NT - 1] = ld_tr_operand<D>(Zc, 32 * qh, mb * 16, c16, g);
+        };
+        read_ops(opd[0], 0);
+        read_ops(opd[1], 1);
+        __builtin_amdgcn_sched_barrier(0);
 
         // S = Q K^T and dP = dO V^T for this wave's 32 queries x 32 keys, one
         // 16 x 16 block at a time: s holds queries 4g+i of query block mq for
@@ -513,24 +537,24 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
                 }
                 dkdv_probs<MASK>(sv, dpv, l2[mq], dd[mq], c, q0 + 32 * qh + mq * 16, g,
                                  k0w + kb * 16 + c16, mq, tf[kb], rf[kb]);
+                fill_piece(nxt2, qt + 2, AT_START + mq * 2 + kb);
             }
         }
-        // dV^T[dv][key] += dO^T r ; dK^T += Q^T t ; C^T += Z^T r.
+        // dV^T[dv][key] += dO^T r ; dK^T += Q^T t ; C^T += Z^T r.  The A operands
+        // of column block mb + 2 are read from LDS while block mb multiplies.
         __builtin_amdgcn_s_setprio(0);
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
-            const bf16x8 ua = ld_tr_operand<D>(Uc, 32 * qh, mb * 16, c16, g);
-            const bf16x8 qa = ld_tr_operand<D>(Qc, 32 * qh, mb * 16, c16, g);
+            const bf16x8* o = opd[mb & 1];
+            const bf16x8 ua = o[0], qa = o[1], za = o[NT - 1];
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
                 accV[kb][mb] = mfma_16x16x32(ua, rf[kb], accV[kb][mb]);
                 accK[kb][mb] = mfma_16x16x32(qa, tf[kb], accK[kb][mb]);
+                if (GPROJ) accC[kb][mb] = mfma_16x16x32(za, rf[kb], accC[kb][mb]);
             }
-            if (GPROJ) {
-                const bf16x8 za = ld_tr_operand<D>(Zc, 32 * qh, mb * 16, c16, g);
-#pragma unroll
-                for (int kb = 0; kb < 2; ++kb) accC[kb][mb] = mfma_16x16x32(za, rf[kb], accC[kb][mb]);
-            }
+            if (mb + 2 < MB) read_ops(opd[mb & 1], mb + 2);
+            fill_piece(nxt2, qt + 2, AT_START + 4 + mb);
         }
         // Tile qt + 1 must have landed; tile qt + 2 may stay in flight.
         wait_vm_lgkm0<FILL_VM>();

@@ -88,14 +88,16 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 // assembly so that the compiler's wait-count insertion does not see them: its
 // alias tracking of LDS DMA targets is imprecise and would wait for every
 // outstanding tile load before each LDS read.  The kernels therefore order
-// these loads themselves, with explicit vmcnt waits and barriers.  The s_nop
-// covers the M0-write to LDS-DMA hazard.
+// these loads themselves, with explicit vmcnt waits and barriers (volatile
+// assembly keeps its place relative to those).  No memory clobber: nothing
+// the compiler reads or writes in LDS overlaps an in-flight DMA target, and a
+// clobber would pin every LDS read of the step between the pieces of a fill.
+// The s_nop covers the M0-write to LDS-DMA hazard.
 __device__ __forceinline__ void lds_dma16(i32x4 desc, uint32_t m0, uint32_t voff) {
 #if defined(__HIP_DEVICE_COMPILE__)
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                  :
-                 : "s"(m0), "v"(voff), "s"(desc)
-                 : "memory");
+                 : "s"(m0), "v"(voff), "s"(desc));
 #else
     (void)desc; (void)m0; (void)voff;
 #endif
@@ -104,8 +106,7 @@ __device__ __forceinline__ void lds_dma4(i32x4 desc, uint32_t m0, uint32_t voff)
 #if defined(__HIP_DEVICE_COMPILE__)
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
                  :
-                 : "s"(m0), "v"(voff), "s"(desc)
-                 : "memory");
+                 : "s"(m0), "v"(voff), "s"(desc));
 #else
     (void)desc; (void)m0; (void)voff;
 #endif
@@ -148,6 +149,14 @@ struct TileDma {
         const uint32_t base = lds_addr(dst);
 #pragma unroll
         for (int k = 0; k < CALLS; ++k) lds_dma16(desc, base + lds[k], voff[k]);
+    }
+    // Call k alone of load(): lets a kernel spread one tile's loads over a step.
+    __device__ __forceinline__ void load_call(const uint16_t* head, uint16_t* dst, int row0, int N,
+                                              bool valid, int k) const {
+        const int r0 = valid ? row0 : 0;
+        const i32x4 desc =
+            buf_desc(head + (size_t)r0 * D, valid ? (uint32_t)(N - r0) * (2 * D) : 0u);
+        lds_dma16(desc, lds_addr(dst) + lds[k], voff[k]);
     }
 };
 
