@@ -105,12 +105,13 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     constexpr int MB = D / 16;  // 16-column blocks of d
     constexpr int KC = D / 32;  // 32-wide k chunks of d
     constexpr int PER_NB = 2 * MB * 4 + 2;  // partial A, B (interleaved) and rho, m
-    // Double-buffered K and V tiles (row-major, swizzled); reused at the end
-    // for the pairwise reduction.
-    // Two separate LDS objects per buffer so the compiler can tell the tile
-    // being read from the one the DMA is filling.
-    __shared__ __attribute__((aligned(16))) uint16_t KV0[2][kTile * D];  // [K, V], buffer 0
-    __shared__ __attribute__((aligned(16))) uint16_t KV1[2][kTile * D];  // [K, V], buffer 1
+    // A three-slot ring of [K tile, V tile] (row-major, swizzled): while tile
+    // i is computed on, tiles i+1 and i+2 are in flight.  Slot 0 is reused at
+    // the end for the pairwise reduction.
+    constexpr int TILE_E = kTile * D;
+    __shared__ __attribute__((aligned(16))) uint16_t S0[2 * TILE_E];
+    __shared__ __attribute__((aligned(16))) uint16_t S1[2 * TILE_E];
+    __shared__ __attribute__((aligned(16))) uint16_t S2[2 * TILE_E];
 
     const int T = (N + kTile - 1) / kTile;
     int bh, tile;
@@ -176,40 +177,36 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     // (their P is 0 and they are not stored).
     const int nplain = (causal || (N % kTile)) ? nkv - 1 : nkv;
 
-    // Rows beyond N are never written by the DMA: zero both buffers once so
-    // every value a product can read is finite.
-    {
-        u32x4* z0 = reinterpret_cast<u32x4*>(&KV0[0][0]);
-        u32x4* z1 = reinterpret_cast<u32x4*>(&KV1[0][0]);
-        constexpr int n16 = (int)(sizeof(KV0) / 16);
-#pragma unroll
-        for (int i = tid; i < n16; i += kThreads) {
-            z0[i] = u32x4{0u, 0u, 0u, 0u};
-            z1[i] = u32x4{0u, 0u, 0u, 0u};
-        }
-    }
-    __syncthreads();
-
     TileDma<D> dma;
     dma.init(lane, wave);
-    dma.load(K + hoff, KV0[0], 0, N);
-    dma.load(V + hoff, KV0[1], 0, N);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    // One key tile: compute on (Kc, Vc) while the DMA fills (Kn, Vn) with the
-    // next tile.
-    auto step = [&](auto masked, int kt, const uint16_t* Kc, const uint16_t* Vc, uint16_t* Kn,
-                    uint16_t* Vn) {
+    // Piece j of the fill of `slot` with key tile kt (K calls, then V calls);
+    // past the last tile it is a zero fill, so every step issues FILL_VM loads.
+    constexpr int FILL_VM = 2 * TileDma<D>::CALLS;
+    auto fill_piece = [&](uint16_t* slot, int kt, int j) {
+        if (j < FILL_VM) {
+            const int t = j / TileDma<D>::CALLS, k = j % TileDma<D>::CALLS;
+            dma.load_call(t ? V + hoff : K + hoff, slot + t * TILE_E, kt * kTile, N, kt < nkv, k);
+        }
+    };
+    // The register operands above must have arrived before the first fill: the
+    // compiler cannot count the fills, so it must have nothing left to wait
+    // for inside the loop.
+    wait_vm_lgkm0<0>();
+#pragma unroll
+    for (int j = 0; j < FILL_VM; ++j) fill_piece(S0, 0, j);
+#pragma unroll
+    for (int j = 0; j < FILL_VM; ++j) fill_piece(S1, 1, j);
+    wait_vm_lgkm0<FILL_VM>();
+    __builtin_amdgcn_s_barrier();
+    // One key tile: compute on slot `cur` while the fill of tile kt + 2 into
+    // `nxt2` is issued piece by piece; at the end tile kt + 1 has landed and
+    // every wave is done with `cur`, which the next step refills.
+    auto step = [&](auto masked, int kt, const uint16_t* cur, uint16_t* nxt2) {
         constexpr bool MASK = decltype(masked)::value;
         const int k0 = kt * kTile;
-        if (kt + 1 < nkv) {
-            dma.load(K + hoff, Kn, k0 + kTile, N);
-            dma.load(V + hoff, Vn, k0 + kTile, N);
-        }
-        // Keep the loads of the next tile at the top of the step: left alone,
-        // the scheduler sinks them next to the closing wait, which exposes
-        // their whole latency.
-        __builtin_amdgcn_sched_barrier(0);
+        const uint16_t* Kc = cur;
+        const uint16_t* Vc = cur + TILE_E;
+        fill_piece(nxt2, kt + 2, 0);
         // S^T = K Q^T and dP^T = V dO^T for this wave's 32 keys x 32 queries:
         // s[nb][kb] holds keys 4g+i of key block kb for query block nb.
         // Raise this wave's issue priority while it feeds the matrix core, so
@@ -234,6 +231,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
                     dp[nb][kb] = mfma_16x16x32(va, uf[nb][kc], dp[nb][kb]);
                 }
             }
+            fill_piece(nxt2, kt + 2, 1 + kb);
         }
         bf16x8 tf[2], rf[2];
 #pragma unroll
@@ -251,6 +249,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
                 accA[nb][mb] = mfma_16x16x32(ka, tf[nb], accA[nb][mb]);
                 if (GPROJ) accB[nb][mb] = mfma_16x16x32(ka, rf[nb], accB[nb][mb]);
             }
+            fill_piece(nxt2, kt + 2, 3 + mb);
         }
         if (GPROJ) {
 #pragma unroll
@@ -259,22 +258,32 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
                 accM[nb] = mfma_16x16x32(ones, rf[nb], accM[nb]);
             }
         }
-        __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the next tile
-        __syncthreads();
+        // Tile kt + 1 must have landed; tile kt + 2 may stay in flight.
+        wait_vm_lgkm0<FILL_VM>();
+        __builtin_amdgcn_s_barrier();
     };
     const std::false_type plain;
     const std::true_type masked;
+    // Tile t lives in slot t mod 3; only the last tile can need masks.
     int kt = 0;
-    for (; kt + 1 < nplain; kt += 2) {
-        step(plain, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
-        step(plain, kt + 1, KV1[0], KV1[1], KV0[0], KV0[1]);
+    for (; kt < nplain; kt += 3) {
+        step(plain, kt, S0, S2);
+        if (kt + 1 < nplain) step(plain, kt + 1, S1, S0);
+        if (kt + 2 < nplain) step(plain, kt + 2, S2, S1);
     }
-    if (kt < nplain) {
-        step(plain, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
-        if (kt + 1 < nkv) step(masked, kt + 1, KV1[0], KV1[1], KV0[0], KV0[1]);
-    } else if (kt < nkv) {
-        step(masked, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
+    if (nplain < nkv) {
+        const int r = nplain % 3;
+        if (r == 0)
+            step(masked, nplain, S0, S2);
+        else if (r == 1)
+            step(masked, nplain, S1, S0);
+        else
+            step(masked, nplain, S2, S1);
     }
+    // The zero fills issued by the last steps must land before slot 0 is
+    // reused for the reduction.
+    wait_vm_lgkm0<0>();
+    __builtin_amdgcn_s_barrier();
 
     // Add the partials of the two waves that own the same queries (one query
     // block at a time, to bound the LDS the exchange needs).
@@ -291,8 +300,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
         red[nb][2 * MB * 4] = accR[nb][0];
         red[nb][2 * MB * 4 + 1] = accM[nb][0];
         if (nb) __syncthreads();  // the previous exchange has been read
-        pair_reduce<PER_NB, sizeof(KV0) / 4>(red[nb], reinterpret_cast<float*>(&KV0[0][0]), wave,
-                                             lane);
+        pair_reduce<PER_NB, sizeof(S0) / 4>(red[nb], reinterpret_cast<float*>(S0), wave, lane);
     }
     if (wave >= 2) return;
 
