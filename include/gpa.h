@@ -84,7 +84,9 @@ gpa_status gpa_attn_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
 /*
  * Workspace bytes gpa_attn_bwd needs for this shape and mode (> 0 for valid
  * shapes, 0 for invalid arguments).  The caller allocates it; its contents on
- * entry do not matter.
+ * entry do not matter.  It holds the FP32 row statistics D, rho, m, lambda
+ * ([B,H,N] each), a per-64-row-tile copy of log2-scaled LSE and D for the
+ * key-major pass, and in gproj mode the BF16 [B,H,N,d] tensor z = BF16(lambda q).
  */
 size_t gpa_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d, int mode);
 
@@ -93,7 +95,8 @@ size_t gpa_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d, 
  * In : Q, K, V, O, dO [B,H,N,d] BF16; LSE [B,H,N] FP32 -- O and LSE as written
  *      by gpa_attn_fwd with the same causal and scale.
  * Out: dQ, dK, dV [B,H,N,d] BF16.
- *   D_i   = sum_c fl32(dO_ic O_ic)                         (preprocess)
+ *   D_i   = sum_c fl32(dO_ic O_ic)     (Algorithm 1's preprocessing, fused
+ *                                        into the query-major pass)
  *   P_ij  = exp(scale x_ij - LSE_i) masked, r = BF16(P),
  *   t_ij  = BF16( fl32[ P_ij (dP_ij - D_i) ] ), dP = dO V^T
  *   dV    = BF16( r^T dO )                                   (every mode)
