@@ -19,7 +19,11 @@
  * Conventions shared by every entry point
  *   Layout   Q, K, V, O, dO, dQ, dK, dV are [B, H, N, d] contiguous, d innermost,
  *            BF16 passed as raw 16-bit patterns (uint16_t).  LSE is FP32 [B, H, N].
- *            Multi-head attention (H query heads = H key/value heads).
+ *            The plain entry points are multi-head attention (H query heads =
+ *            H key/value heads); the *_gqa ones take grouped-query attention:
+ *            Q, O, dO, dQ, LSE have Hq heads, K, V, dK, dV have Hkv heads,
+ *            Hq a multiple of Hkv, and query head h reads key/value head
+ *            h / (Hq / Hkv) (consecutive query heads share one).
  *   Shapes   B, H, N >= 1; d in {64, 128}; B*H*N*d < 2^31.
  *   Causal   causal != 0 means query i attends to keys j <= i (square N x N).
  *   Scale    alpha (the attention scale), finite and > 0; usually 1/sqrt(d).
@@ -128,6 +132,38 @@ gpa_status gpa_attn_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
 gpa_status gpa_bwd_stats_offsets(int64_t B, int64_t H, int64_t N, int64_t d, int mode,
                                  size_t* off_D, size_t* off_rho, size_t* off_m,
                                  size_t* off_lambda);
+
+/*
+ * Grouped-query attention (Section 3.2, eq. row-gradients: key and value
+ * gradients also sum over the query heads that share a KV head; appendix
+ * "Gauge Projection: Proofs", "Rounding in the implemented key correction":
+ * GQA only enlarges the set of query rows contributing to a key).  Same
+ * arithmetic as gpa_attn_fwd / gpa_attn_bwd per query head; shapes as in the
+ * Layout convention with Hq query and Hkv key/value heads.  In the backward,
+ * lambda and z stay per query-head row, and for each key/value head
+ *   dV = BF16( sum_h r_h^T dO_h ),
+ *   dK = BF16( fl32[ scale * sum_h fl32(t_h^T Q_h - r_h^T z_h) ] )   (gproj;
+ *        without the r^T z term in plain and gproj_q),
+ * the per-head FP32 terms added in head order (deterministic).  With
+ * Hq == Hkv these are exactly gpa_attn_fwd / gpa_attn_bwd.  The workspace
+ * (gpa_attn_bwd_gqa_workspace_bytes) begins with the layout gpa_bwd_stats_offsets
+ * reports for B, H = Hq.  Errors as for the multi-head entry points, plus
+ * GPA_EINVAL when Hq is not a positive multiple of Hkv.
+ */
+gpa_status gpa_attn_fwd_gqa(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                            uint16_t* O, float* LSE,
+                            int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t d,
+                            int causal, float scale, void* stream);
+
+size_t gpa_attn_bwd_gqa_workspace_bytes(int64_t B, int64_t Hq, int64_t Hkv, int64_t N,
+                                        int64_t d, int mode);
+
+gpa_status gpa_attn_bwd_gqa(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                            const uint16_t* O, const float* LSE, const uint16_t* dO,
+                            uint16_t* dQ, uint16_t* dK, uint16_t* dV,
+                            int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t d,
+                            int causal, float scale, int mode,
+                            void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * FP32 attention baseline (the accuracy class of the paper's "FP32 attention",

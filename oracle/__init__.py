@@ -6,7 +6,9 @@ CPU-baseline leg of ``bench.py`` import this package.  The product library
 this package shares no code with it.
 
 Contents
-  exact(...)            FP64 exact attention forward + VJP (C, OpenMP), the
+  exact(...)            FP64 exact attention forward + VJP (C, OpenMP; also
+                        grouped-query attention when k, v have fewer heads
+                        than q, key/value gradients summed over each group), the
                         accuracy target: the paper measures errors against the
                         exact VJP in FP64 on the same BF16 inputs (Section 3.2,
                         and the appendix "Reference and metric").
@@ -47,6 +49,9 @@ def _load():
     lib.oracle_attention_f64.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
                                          ctypes.c_int, ctypes.c_double,
                                          dp, dp, dp, dp, dp, dp, dp, dp, dp, ctypes.c_int]
+    lib.oracle_attention_gqa_f64.restype = ctypes.c_int
+    lib.oracle_attention_gqa_f64.argtypes = [ctypes.c_int64] * 5 + [ctypes.c_int, ctypes.c_double] \
+        + [dp] * 9 + [ctypes.c_int]
     lib.oracle_max_threads.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -74,10 +79,15 @@ def exact(q, k, v, do, causal: bool, scale: float, nthreads: int = 0):
 
     q, k, v, do: arrays [..., N, d] (uint16 BF16 bits or floats; any leading
     dims, flattened to heads).  Returns a dict with float64 arrays O, LSE,
-    dQ, dK, dV of the matching shapes (LSE without the d axis).
+    dQ, dK, dV of the matching shapes (LSE without the d axis).  With 4-D
+    [B, Hq, N, d] q, do and [B, Hkv, N, d] k, v (Hkv dividing Hq, fewer heads)
+    it computes grouped-query attention: query head h reads key/value head
+    h // (Hq // Hkv), and dK, dV are shaped like k, v.
     """
     lib = _load()
     Q, K, V, U = (as_f64(t) for t in (q, k, v, do))
+    if Q.ndim == 4 and K.ndim == 4 and K.shape[1] != Q.shape[1]:
+        return _exact_gqa(lib, Q, K, V, U, causal, scale, nthreads)
     shape = Q.shape
     N, d = shape[-2], shape[-1]
     BH = int(np.prod(shape[:-2])) if len(shape) > 2 else 1
@@ -96,6 +106,27 @@ def exact(q, k, v, do, causal: bool, scale: float, nthreads: int = 0):
         raise RuntimeError(f"oracle_attention_f64 failed with code {rc}")
     return dict(O=O.reshape(shape), LSE=LSE.reshape(shape[:-1]), dQ=dQ.reshape(shape),
                 dK=dK.reshape(shape), dV=dV.reshape(shape))
+
+
+def _exact_gqa(lib, Q, K, V, U, causal, scale, nthreads):
+    B, Hq, N, d = Q.shape
+    Hkv = K.shape[1]
+    if K.shape != (B, Hkv, N, d) or V.shape != K.shape or U.shape != Q.shape or Hq % Hkv:
+        raise ValueError("grouped-query shapes: q, do [B, Hq, N, d]; k, v [B, Hkv, N, d]")
+    Q, K, V, U = (np.ascontiguousarray(t) for t in (Q, K, V, U))
+    O = np.empty_like(Q)
+    LSE = np.empty((B, Hq, N))
+    dQ = np.empty_like(Q)
+    dK = np.empty_like(K)
+    dV = np.empty_like(K)
+    dp = ctypes.POINTER(ctypes.c_double)
+    ptr = lambda a: a.ctypes.data_as(dp)  # noqa: E731
+    rc = lib.oracle_attention_gqa_f64(B, Hq, Hkv, N, d, int(bool(causal)), float(scale),
+                                      ptr(Q), ptr(K), ptr(V), ptr(U), ptr(O), ptr(LSE),
+                                      ptr(dQ), ptr(dK), ptr(dV), int(nthreads))
+    if rc != 0:
+        raise RuntimeError(f"oracle_attention_gqa_f64 failed with code {rc}")
+    return dict(O=O, LSE=LSE, dQ=dQ, dK=dK, dV=dV)
 
 
 def rel_l2(approx, target) -> float:

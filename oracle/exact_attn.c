@@ -176,6 +176,52 @@ int oracle_attention_f64(int64_t BH, int64_t N, int64_t d, int causal, double al
     return 0;
 }
 
+/*
+ * Grouped-query attention: Q, dO, O, dQ are [B][Hq][N][d], K, V, dK, dV are
+ * [B][Hkv][N][d], LSE is [B][Hq][N], and query head h of batch b reads key/value
+ * head h / (Hq / Hkv).  Each query head's VJP is the multi-head one above; the
+ * key and value gradients of a key/value head are the sums of its query heads'
+ * contributions (paper, Section 3.2 after eq. row-gradients: key and value
+ * contributions also sum over the query heads that share a KV head), added in
+ * head order.  Returns 0, 1 (allocation failure) or 2 (bad arguments).
+ */
+int oracle_attention_gqa_f64(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t d, int causal,
+                             double alpha, const double* Q, const double* K, const double* V,
+                             const double* dO, double* O, double* LSE, double* dQ, double* dK,
+                             double* dV, int nthreads) {
+    if (B < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || N < 0 || d < 1) return 2;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+    const int64_t G = Hq / Hkv, hd = N * d;
+    memset(dK, 0, (size_t)(B * Hkv * hd) * sizeof(double));
+    memset(dV, 0, (size_t)(B * Hkv * hd) * sizeof(double));
+    if (N == 0) return 0;
+    double* tk = malloc((size_t)hd * sizeof(double));
+    double* tv = malloc((size_t)hd * sizeof(double));
+    if (!tk || !tv) {
+        free(tk); free(tv);
+        return 1;
+    }
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t h = 0; h < Hq; ++h) {
+            const int64_t qh = b * Hq + h, kh = b * Hkv + h / G;
+            if (one_head(N, d, causal, alpha, Q + qh * hd, K + kh * hd, V + kh * hd, dO + qh * hd,
+                         O + qh * hd, LSE + qh * N, dQ + qh * hd, tk, tv)) {
+                free(tk); free(tv);
+                return 1;
+            }
+            for (int64_t e = 0; e < hd; ++e) {
+                dK[kh * hd + e] += tk[e];
+                dV[kh * hd + e] += tv[e];
+            }
+        }
+    free(tk); free(tv);
+    return 0;
+}
+
 int oracle_max_threads(void) {
 #ifdef _OPENMP
     return omp_get_max_threads();

@@ -12,6 +12,9 @@ Python names mirror the C entry points:
   gpa_attn_bwd_workspace_bytes / attn_bwd_workspace_bytes
   gpa_bwd_stats_offsets / bwd_stats_offsets
   gpa_fp32_attn / fp32_attn               -> O, LSE, dQ, dK, dV (FP32 baseline)
+Grouped-query attention (k, v with fewer heads than q) goes through
+gpa_attn_fwd_gqa / gpa_attn_bwd_gqa / gpa_attn_bwd_gqa_workspace_bytes; the
+same Python functions pick them from the tensor shapes.
 """
 from __future__ import annotations
 
@@ -62,6 +65,13 @@ def lib():
     L.gpa_attn_bwd_workspace_bytes.argtypes = [I64, I64, I64, I64, INT]
     L.gpa_attn_bwd.restype = INT
     L.gpa_attn_bwd.argtypes = [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, INT, F32, INT, P, SZ, P]
+    L.gpa_attn_fwd_gqa.restype = INT
+    L.gpa_attn_fwd_gqa.argtypes = [P, P, P, P, P, I64, I64, I64, I64, I64, INT, F32, P]
+    L.gpa_attn_bwd_gqa_workspace_bytes.restype = SZ
+    L.gpa_attn_bwd_gqa_workspace_bytes.argtypes = [I64, I64, I64, I64, I64, INT]
+    L.gpa_attn_bwd_gqa.restype = INT
+    L.gpa_attn_bwd_gqa.argtypes = [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, I64, INT, F32,
+                                   INT, P, SZ, P]
     L.gpa_bwd_stats_offsets.restype = INT
     L.gpa_bwd_stats_offsets.argtypes = [I64, I64, I64, I64, INT] + [ctypes.POINTER(SZ)] * 4
     L.gpa_fp32_attn_workspace_bytes.restype = SZ
@@ -108,21 +118,43 @@ def _scale(d: int, scale):
     return 1.0 / math.sqrt(d) if scale is None else float(scale)
 
 
+def _kv_heads(q, k, name="k"):
+    B, Hq, N, d = _shape(q)
+    if k.dim() != 4 or k.shape[0] != B or k.shape[2] != N or k.shape[3] != d:
+        raise ValueError(f"{name} must be [B, Hkv, N, d] matching q, got {tuple(k.shape)}")
+    Hkv = int(k.shape[1])
+    if Hkv < 1 or Hq % Hkv:
+        raise ValueError(f"query heads {Hq} must be a multiple of key/value heads {Hkv}")
+    return Hkv
+
+
 def attn_fwd(q, k, v, causal: bool = True, scale=None):
-    """FA3-SBS forward.  q, k, v: bf16 [B, H, N, d] on the GPU.
-    Returns O (bf16, same shape) and LSE (float32 [B, H, N])."""
+    """FA3-SBS forward.  q: bf16 [B, Hq, N, d]; k, v: bf16 [B, Hkv, N, d] on the
+    GPU (Hkv == Hq: multi-head; Hkv < Hq: grouped-query).
+    Returns O (bf16, shaped like q) and LSE (float32 [B, Hq, N])."""
     B, H, N, d = _shape(q)
-    for t, n in ((q, "q"), (k, "k"), (v, "v")):
-        _need(t, n, (B, H, N, d), torch.bfloat16)
+    Hkv = _kv_heads(q, k)
+    _need(q, "q", (B, H, N, d), torch.bfloat16)
+    for t, n in ((k, "k"), (v, "v")):
+        _need(t, n, (B, Hkv, N, d), torch.bfloat16)
     o = torch.empty_like(q)
     lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
-    _check(lib().gpa_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
-                              B, H, N, d, int(bool(causal)), _scale(d, scale), _stream(q)))
+    if Hkv == H:
+        _check(lib().gpa_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                  lse.data_ptr(), B, H, N, d, int(bool(causal)), _scale(d, scale),
+                                  _stream(q)))
+    else:
+        _check(lib().gpa_attn_fwd_gqa(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                      lse.data_ptr(), B, H, Hkv, N, d, int(bool(causal)),
+                                      _scale(d, scale), _stream(q)))
     return o, lse
 
 
-def attn_bwd_workspace_bytes(B: int, H: int, N: int, d: int, mode="gproj") -> int:
-    return int(lib().gpa_attn_bwd_workspace_bytes(B, H, N, d, MODES[mode] if isinstance(mode, str) else int(mode)))
+def attn_bwd_workspace_bytes(B: int, H: int, N: int, d: int, mode="gproj", Hkv=None) -> int:
+    m = MODES[mode] if isinstance(mode, str) else int(mode)
+    if Hkv is None or Hkv == H:
+        return int(lib().gpa_attn_bwd_workspace_bytes(B, H, N, d, m))
+    return int(lib().gpa_attn_bwd_gqa_workspace_bytes(B, H, Hkv, N, d, m))
 
 
 def bwd_stats_offsets(B: int, H: int, N: int, d: int, mode="gproj"):
@@ -135,25 +167,36 @@ def bwd_stats_offsets(B: int, H: int, N: int, d: int, mode="gproj"):
 
 def attn_bwd(q, k, v, o, lse, do, mode: str = "gproj", causal: bool = True, scale=None,
              workspace=None, return_stats: bool = False):
-    """Backward (plain | gproj_q | gproj).  Returns dQ, dK, dV (bf16); with
-    return_stats=True also a dict of FP32 [B, H, N] tensors D, rho, m, lambda
-    (views into the workspace)."""
+    """Backward (plain | gproj_q | gproj).  q, o, do: bf16 [B, Hq, N, d];
+    k, v: bf16 [B, Hkv, N, d].  Returns dQ, dK, dV (bf16, shaped like q, k, v);
+    with return_stats=True also a dict of FP32 [B, Hq, N] tensors D, rho, m,
+    lambda (views into the workspace)."""
     B, H, N, d = _shape(q)
-    for t, n in ((q, "q"), (k, "k"), (v, "v"), (o, "o"), (do, "do")):
+    Hkv = _kv_heads(q, k)
+    for t, n in ((q, "q"), (o, "o"), (do, "do")):
         _need(t, n, (B, H, N, d), torch.bfloat16)
+    for t, n in ((k, "k"), (v, "v")):
+        _need(t, n, (B, Hkv, N, d), torch.bfloat16)
     _need(lse, "lse", (B, H, N), torch.float32)
     mcode = MODES[mode] if isinstance(mode, str) else int(mode)
-    nbytes = int(lib().gpa_attn_bwd_workspace_bytes(B, H, N, d, mcode))
+    nbytes = attn_bwd_workspace_bytes(B, H, N, d, mcode, Hkv)
     if workspace is None:
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
     dq = torch.empty_like(q)
-    dk = torch.empty_like(q)
-    dv = torch.empty_like(q)
-    _check(lib().gpa_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(),
-                              do.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
-                              B, H, N, d, int(bool(causal)), _scale(d, scale), mcode,
-                              workspace.data_ptr(), workspace.numel() * workspace.element_size(),
-                              _stream(q)))
+    dk = torch.empty_like(k)
+    dv = torch.empty_like(v)
+    wsz = workspace.numel() * workspace.element_size()
+    if Hkv == H:
+        _check(lib().gpa_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                  lse.data_ptr(), do.data_ptr(), dq.data_ptr(), dk.data_ptr(),
+                                  dv.data_ptr(), B, H, N, d, int(bool(causal)), _scale(d, scale),
+                                  mcode, workspace.data_ptr(), wsz, _stream(q)))
+    else:
+        _check(lib().gpa_attn_bwd_gqa(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                      lse.data_ptr(), do.data_ptr(), dq.data_ptr(), dk.data_ptr(),
+                                      dv.data_ptr(), B, H, Hkv, N, d, int(bool(causal)),
+                                      _scale(d, scale), mcode, workspace.data_ptr(), wsz,
+                                      _stream(q)))
     if not return_stats:
         return dq, dk, dv
     offs = bwd_stats_offsets(B, H, N, d, mcode)

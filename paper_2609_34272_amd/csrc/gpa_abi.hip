@@ -109,17 +109,21 @@ gpa_status launched(hipError_t e, const char* what) {
 }
 
 struct BwdLayout {
-    size_t D, rho, m, lam, ts, z, total;
+    size_t D, rho, m, lam, ts, z, dkp, dvp, total;
 };
 
-// Four FP32 [B,H,N] row statistics; per 64-row query tile a 512-byte block of
-// log2-scaled LSE and D (FP32 [B*H, T, 2, 64], T = N rounded up to 64, over 64)
-// that the key-major pass stages with the tile; then (gproj mode only) the
-// BF16 [B,H,N,d] tensor z = BF16(lambda q) that the key correction contracts.
-BwdLayout bwd_layout(int64_t B, int64_t H, int64_t N, int64_t d, int mode) {
-    const size_t row = round_up((size_t)B * H * N * sizeof(float));
+// Four FP32 [B,Hq,N] row statistics; per 64-row query tile a 512-byte block of
+// log2-scaled LSE and D (FP32 [B*Hq, T, 2, 64], T = N rounded up to 64, over
+// 64) that the key-major pass stages with the tile; then (gproj mode only) the
+// BF16 [B,Hq,N,d] tensor z = BF16(lambda q) that the key correction
+// contracts; then, for grouped-query attention (Hq > Hkv) only, the FP32
+// [B,Hq,N,d] per-query-head contributions to dK and dV that the group sum
+// adds.
+BwdLayout bwd_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t d, int mode) {
+    const size_t row = round_up((size_t)B * Hq * N * sizeof(float));
     const size_t T = (size_t)(N + 63) / 64;
-    const size_t tstats = round_up((size_t)B * H * T * 128 * sizeof(float));
+    const size_t tstats = round_up((size_t)B * Hq * T * 128 * sizeof(float));
+    const size_t part = Hq > Hkv ? round_up((size_t)B * Hq * N * d * sizeof(float)) : 0;
     BwdLayout L;
     L.D = 0;
     L.rho = row;
@@ -127,8 +131,17 @@ BwdLayout bwd_layout(int64_t B, int64_t H, int64_t N, int64_t d, int mode) {
     L.lam = 3 * row;
     L.ts = 4 * row;
     L.z = L.ts + tstats;
-    L.total = L.z + (mode == 2 ? round_up((size_t)B * H * N * d * 2) : 0);
+    L.dkp = L.z + (mode == 2 ? round_up((size_t)B * Hq * N * d * 2) : 0);
+    L.dvp = L.dkp + part;
+    L.total = L.dvp + part;
     return L;
+}
+
+gpa_status check_heads(int64_t Hq, int64_t Hkv) {
+    if (Hkv < 1 || Hq < 1 || Hq % Hkv != 0)
+        return fail(GPA_EINVAL, "query heads %lld must be a positive multiple of key/value heads %lld",
+                    (long long)Hq, (long long)Hkv);
+    return GPA_OK;
 }
 
 }  // namespace
@@ -150,25 +163,38 @@ const char* gpa_status_str(gpa_status s) {
 
 const char* gpa_last_error(void) { return g_last_error.c_str(); }
 
-gpa_status gpa_attn_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, uint16_t* O,
-                        float* LSE, int64_t B, int64_t H, int64_t N, int64_t d, int causal,
-                        float scale, void* stream) {
-    gpa_status s = check_shape(B, H, N, d, scale);
+gpa_status gpa_attn_fwd_gqa(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                            uint16_t* O, float* LSE, int64_t B, int64_t Hq, int64_t Hkv,
+                            int64_t N, int64_t d, int causal, float scale, void* stream) {
+    gpa_status s = check_shape(B, Hq, N, d, scale);
     if (s != GPA_OK) return s;
-    const size_t tb = (size_t)B * H * N * d * 2, lb = (size_t)B * H * N * 4;
-    s = check_ptrs({{Q, tb, "Q"}, {K, tb, "K"}, {V, tb, "V"}}, {{O, tb, "O"}, {LSE, lb, "LSE"}});
+    if ((s = check_heads(Hq, Hkv)) != GPA_OK) return s;
+    const size_t tq = (size_t)B * Hq * N * d * 2, tkv = (size_t)B * Hkv * N * d * 2;
+    const size_t lb = (size_t)B * Hq * N * 4;
+    s = check_ptrs({{Q, tq, "Q"}, {K, tkv, "K"}, {V, tkv, "V"}}, {{O, tq, "O"}, {LSE, lb, "LSE"}});
     if (s != GPA_OK) return s;
-    const gpa::Shape sh{(int)(B * H), (int)N, (int)d, causal ? 1 : 0, scale};
+    const gpa::Shape sh{(int)(B * Hq), (int)N, (int)d, causal ? 1 : 0, scale, (int)(Hq / Hkv)};
     hipStream_t st = (hipStream_t)stream;
     return launched(timed(gpa::kKFwd, st, [&] { return gpa::launch_fwd(Q, K, V, O, LSE, sh, st); }),
                     "fwd_sbs");
 }
 
-size_t gpa_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d, int mode) {
+gpa_status gpa_attn_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, uint16_t* O,
+                        float* LSE, int64_t B, int64_t H, int64_t N, int64_t d, int causal,
+                        float scale, void* stream) {
+    return gpa_attn_fwd_gqa(Q, K, V, O, LSE, B, H, H, N, d, causal, scale, stream);
+}
+
+size_t gpa_attn_bwd_gqa_workspace_bytes(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t d,
+                                        int mode) {
     if (mode < 0 || mode > 2) return 0;
-    if (B < 1 || H < 1 || N < 1 || (d != 64 && d != 128)) return 0;
-    if ((double)B * H * N * d >= 2147483648.0) return 0;
-    return bwd_layout(B, H, N, d, mode).total;
+    if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || N < 1 || (d != 64 && d != 128)) return 0;
+    if ((double)B * Hq * N * d >= 2147483648.0) return 0;
+    return bwd_layout(B, Hq, Hkv, N, d, mode).total;
+}
+
+size_t gpa_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d, int mode) {
+    return gpa_attn_bwd_gqa_workspace_bytes(B, H, H, N, d, mode);
 }
 
 gpa_status gpa_bwd_stats_offsets(int64_t B, int64_t H, int64_t N, int64_t d, int mode,
@@ -176,7 +202,7 @@ gpa_status gpa_bwd_stats_offsets(int64_t B, int64_t H, int64_t N, int64_t d, int
                                  size_t* off_lambda) {
     if (gpa_attn_bwd_workspace_bytes(B, H, N, d, mode) == 0)
         return fail(GPA_EINVAL, "invalid shape or mode");
-    const BwdLayout L = bwd_layout(B, H, N, d, mode);
+    const BwdLayout L = bwd_layout(B, H, H, N, d, mode);
     if (off_D) *off_D = L.D;
     if (off_rho) *off_rho = L.rho;
     if (off_m) *off_m = L.m;
@@ -184,29 +210,31 @@ gpa_status gpa_bwd_stats_offsets(int64_t B, int64_t H, int64_t N, int64_t d, int
     return GPA_OK;
 }
 
-gpa_status gpa_attn_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                        const uint16_t* O, const float* LSE, const uint16_t* dO, uint16_t* dQ,
-                        uint16_t* dK, uint16_t* dV, int64_t B, int64_t H, int64_t N, int64_t d,
-                        int causal, float scale, int mode, void* workspace,
-                        size_t workspace_bytes, void* stream) {
-    gpa_status s = check_shape(B, H, N, d, scale);
+gpa_status gpa_attn_bwd_gqa(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                            const uint16_t* O, const float* LSE, const uint16_t* dO,
+                            uint16_t* dQ, uint16_t* dK, uint16_t* dV, int64_t B, int64_t Hq,
+                            int64_t Hkv, int64_t N, int64_t d, int causal, float scale, int mode,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+    gpa_status s = check_shape(B, Hq, N, d, scale);
     if (s != GPA_OK) return s;
+    if ((s = check_heads(Hq, Hkv)) != GPA_OK) return s;
     if (mode < 0 || mode > 2) return fail(GPA_EINVAL, "mode %d is not 0, 1 or 2", mode);
-    const size_t need = gpa_attn_bwd_workspace_bytes(B, H, N, d, mode);
+    const size_t need = gpa_attn_bwd_gqa_workspace_bytes(B, Hq, Hkv, N, d, mode);
     if (!workspace || workspace_bytes < need)
         return fail(GPA_EWORKSPACE, "workspace %p of %zu bytes; %zu needed", workspace,
                     workspace_bytes, need);
     if ((uintptr_t)workspace % kAlign)
         return fail(GPA_EWORKSPACE, "workspace is not %zu-byte aligned", kAlign);
-    const size_t tb = (size_t)B * H * N * d * 2, lb = (size_t)B * H * N * 4;
-    s = check_ptrs({{Q, tb, "Q"}, {K, tb, "K"}, {V, tb, "V"}, {O, tb, "O"}, {LSE, lb, "LSE"},
-                    {dO, tb, "dO"}},
-                   {{dQ, tb, "dQ"}, {dK, tb, "dK"}, {dV, tb, "dV"}, {workspace, need, "workspace"}});
+    const size_t tq = (size_t)B * Hq * N * d * 2, tkv = (size_t)B * Hkv * N * d * 2;
+    const size_t lb = (size_t)B * Hq * N * 4;
+    s = check_ptrs({{Q, tq, "Q"}, {K, tkv, "K"}, {V, tkv, "V"}, {O, tq, "O"}, {LSE, lb, "LSE"},
+                    {dO, tq, "dO"}},
+                   {{dQ, tq, "dQ"}, {dK, tkv, "dK"}, {dV, tkv, "dV"}, {workspace, need, "workspace"}});
     if (s != GPA_OK) return s;
 
-    const gpa::Shape sh{(int)(B * H), (int)N, (int)d, causal ? 1 : 0, scale};
+    const gpa::Shape sh{(int)(B * Hq), (int)N, (int)d, causal ? 1 : 0, scale, (int)(Hq / Hkv)};
     hipStream_t st = (hipStream_t)stream;
-    const BwdLayout L = bwd_layout(B, H, N, d, mode);
+    const BwdLayout L = bwd_layout(B, Hq, Hkv, N, d, mode);
     char* ws = (char*)workspace;
     float* Drow = (float*)(ws + L.D);
     float* rho = (float*)(ws + L.rho);
@@ -214,6 +242,8 @@ gpa_status gpa_attn_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
     float* lam = (float*)(ws + L.lam);
     float* tstats = (float*)(ws + L.ts);
     uint16_t* zbuf = mode == 2 ? (uint16_t*)(ws + L.z) : nullptr;
+    float* dkp = sh.G > 1 ? (float*)(ws + L.dkp) : nullptr;
+    float* dvp = sh.G > 1 ? (float*)(ws + L.dvp) : nullptr;
 
     s = launched(timed(gpa::kKBwdDq, st,
                        [&] {
@@ -222,12 +252,25 @@ gpa_status gpa_attn_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                        }),
                  "bwd_dq");
     if (s != GPA_OK) return s;
-    return launched(timed(gpa::kKBwdDkdv, st,
-                          [&] {
-                              return gpa::launch_bwd_dkdv(Q, K, V, dO, tstats, zbuf, dK, dV, mode,
-                                                          sh, st);
-                          }),
-                    "bwd_dkdv");
+    s = launched(timed(gpa::kKBwdDkdv, st,
+                       [&] {
+                           return gpa::launch_bwd_dkdv(Q, K, V, dO, tstats, zbuf, dK, dV, dkp, dvp,
+                                                       mode, sh, st);
+                       }),
+                 "bwd_dkdv");
+    if (s != GPA_OK || sh.G == 1) return s;
+    return launched(timed(gpa::kKGroupSum, st,
+                          [&] { return gpa::launch_bwd_group_sum(dkp, dvp, dK, dV, sh, st); }),
+                    "group_sum");
+}
+
+gpa_status gpa_attn_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                        const uint16_t* O, const float* LSE, const uint16_t* dO, uint16_t* dQ,
+                        uint16_t* dK, uint16_t* dV, int64_t B, int64_t H, int64_t N, int64_t d,
+                        int causal, float scale, int mode, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+    return gpa_attn_bwd_gqa(Q, K, V, O, LSE, dO, dQ, dK, dV, B, H, H, N, d, causal, scale, mode,
+                            workspace, workspace_bytes, stream);
 }
 
 size_t gpa_fp32_attn_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d) {
@@ -253,7 +296,7 @@ gpa_status gpa_fp32_attn(const uint16_t* Q, const uint16_t* K, const uint16_t* V
                    {{O, tb, "O"}, {LSE, lb, "LSE"}, {dQ, tb, "dQ"}, {dK, tb, "dK"},
                     {dV, tb, "dV"}, {workspace, need, "workspace"}});
     if (s != GPA_OK) return s;
-    const gpa::Shape sh{(int)(B * H), (int)N, (int)d, causal ? 1 : 0, scale};
+    const gpa::Shape sh{(int)(B * H), (int)N, (int)d, causal ? 1 : 0, scale, 1};
     hipStream_t st = (hipStream_t)stream;
     float* O32 = (float*)workspace;
     float* Drow = (float*)((char*)workspace + round_up((size_t)B * H * N * d * 4));
@@ -297,8 +340,9 @@ int gpa_profile_read(double* total_ms, int64_t* launches, int n) {
 }
 
 const char* gpa_kernel_name(int id) {
-    static const char* names[gpa::kNumKernels] = {"fwd_sbs",  "bwd_dq",   "bwd_dkdv", "fp32_fwd",
-                                                  "fp32_pre", "fp32_dq", "fp32_dkdv"};
+    static const char* names[gpa::kNumKernels] = {"fwd_sbs",  "bwd_dq",   "bwd_dkdv",
+                                                  "fp32_fwd", "fp32_pre", "fp32_dq",
+                                                  "fp32_dkdv", "group_sum"};
     return (id >= 0 && id < gpa::kNumKernels) ? names[id] : "";
 }
 

@@ -101,7 +101,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     const uint16_t* __restrict__ dO, const float* __restrict__ LSE, float* __restrict__ D_out,
     float* __restrict__ TS, uint16_t* __restrict__ dQ,
     float* __restrict__ rho_out, float* __restrict__ m_out, float* __restrict__ lam_out,
-    uint16_t* __restrict__ Zout, int BH, int N, int causal, float scale) {
+    uint16_t* __restrict__ Zout, int BH, int N, int causal, float scale, int G) {
     constexpr int MB = D / 16;  // 16-column blocks of d
     constexpr int KC = D / 32;  // 32-wide k chunks of d
     constexpr int PER_NB = 2 * MB * 4 + 2;  // partial A, B (interleaved) and rho, m
@@ -116,7 +116,8 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     const int T = (N + kTile - 1) / kTile;
     int bh, tile;
     map_block(blockIdx.x, BH, T, causal != 0, &bh, &tile);
-    const size_t hoff = (size_t)bh * N * D;
+    const size_t hoff = (size_t)bh * N * D;        // query head
+    const size_t kvoff = (size_t)(bh / G) * N * D;  // its key/value head
     const size_t soff = (size_t)bh * N;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -185,7 +186,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     auto fill_piece = [&](uint16_t* slot, int kt, int j) {
         if (j < FILL_VM) {
             const int t = j / TileDma<D>::CALLS, k = j % TileDma<D>::CALLS;
-            dma.load_call(t ? V + hoff : K + hoff, slot + t * TILE_E, kt * kTile, N, kt < nkv, k);
+            dma.load_call(t ? V + kvoff : K + kvoff, slot + t * TILE_E, kt * kTile, N, kt < nkv, k);
         }
     };
     // The register operands above must have arrived before the first fill: the
@@ -385,7 +386,8 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
     const float* __restrict__ TS, const uint16_t* __restrict__ Z, uint16_t* __restrict__ dK,
-    uint16_t* __restrict__ dV, int BH, int N, int causal, float scale) {
+    uint16_t* __restrict__ dV, float* __restrict__ dKp, float* __restrict__ dVp, int BH, int N,
+    int causal, float scale, int G) {
     constexpr int MB = D / 16;
     constexpr int KC = D / 32;
     constexpr int NT = GPROJ ? 3 : 2;  // staged tensors: Q, dO (and Z = BF16(lambda Q))
@@ -406,7 +408,8 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     const int T = (N + kTile - 1) / kTile;
     int bh, tile;
     map_block(blockIdx.x, BH, T, false, &bh, &tile);
-    const size_t hoff = (size_t)bh * N * D;
+    const size_t hoff = (size_t)bh * N * D;        // query head: Q, dO, z, partials
+    const size_t kvoff = (size_t)(bh / G) * N * D;  // its key/value head: K, V, dK, dV
     const float* tsh = TS + (size_t)bh * T * kStatFloats;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -419,8 +422,8 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     // K^T and V^T as B operands: column = this lane's key of block kb, k = d.
     // Rows beyond N load as zero.
     const uint32_t tbytes = (uint32_t)N * (2 * D);
-    const rsrc_t rk = make_rsrc(K + hoff, tbytes);
-    const rsrc_t rv = make_rsrc(V + hoff, tbytes);
+    const rsrc_t rk = make_rsrc(K + kvoff, tbytes);
+    const rsrc_t rv = make_rsrc(V + kvoff, tbytes);
     bf16x8 kf[2][KC], vf[2][KC];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -609,8 +612,27 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     for (int kb = 0; kb < 2; ++kb) {
         const int krow = k0w + kb * 16 + c16;
         if (krow >= N) continue;
-        uint16_t* vrow = dV + hoff + (size_t)krow * D;
-        uint16_t* krw = dK + hoff + (size_t)krow * D;
+        if (G > 1) {
+            // This query head's FP32 contributions; the group sum casts them.
+            float* vp = dVp + hoff + (size_t)krow * D;
+            float* kp = dKp + hoff + (size_t)krow * D;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+                f32x4 dv, dk;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+#pragma clang fp contract(off)
+                    const int j = (mb * 4 + i) * NV;
+                    dv[i] = red[kb][j];
+                    dk[i] = GPROJ ? red[kb][j + 1] - red[kb][j + NV - 1] : red[kb][j + 1];
+                }
+                *reinterpret_cast<f32x4*>(vp + mb * 16 + 4 * g) = dv;
+                *reinterpret_cast<f32x4*>(kp + mb * 16 + 4 * g) = dk;
+            }
+            continue;
+        }
+        uint16_t* vrow = dV + kvoff + (size_t)krow * D;
+        uint16_t* krw = dK + kvoff + (size_t)krow * D;
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
             float dv[4], dk[4];
@@ -632,6 +654,35 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     }
 }
 
+// Group sum of the per-query-head FP32 contributions (G > 1): thread t of the
+// grid owns 4 consecutive elements of one key/value head and adds the G query
+// heads' values in head order; dK takes the scale after the sum, matching
+// BF16(fl32[alpha (dK^acc - C)]) with dK^acc and C summed over the group.
+__global__ __launch_bounds__(256) void group_sum_kernel(const float* __restrict__ dKp,
+                                                        const float* __restrict__ dVp,
+                                                        uint16_t* __restrict__ dK,
+                                                        uint16_t* __restrict__ dV, int BHkv,
+                                                        int G, size_t per_head, float scale) {
+    const size_t quads = per_head / 4;
+    const size_t t = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (size_t)BHkv * quads) return;
+    const size_t kvh = t / quads, e = (t - kvh * quads) * 4;
+    f32x4 sk = {0.f, 0.f, 0.f, 0.f}, sv = {0.f, 0.f, 0.f, 0.f};
+    for (int gq = 0; gq < G; ++gq) {
+        const size_t off = (kvh * G + gq) * per_head + e;
+        sk += *reinterpret_cast<const f32x4*>(dKp + off);
+        sv += *reinterpret_cast<const f32x4*>(dVp + off);
+    }
+    float k4[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma clang fp contract(off)
+        k4[i] = scale * sk[i];
+    }
+    st_bf16x4(dK + kvh * per_head + e, k4[0], k4[1], k4[2], k4[3]);
+    st_bf16x4(dV + kvh * per_head + e, sv[0], sv[1], sv[2], sv[3]);
+}
+
 }  // namespace
 
 hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
@@ -643,7 +694,7 @@ hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V
 #define GPA_DQ(DD, GP, WZ)                                                                   \
     bwd_dq_kernel<DD, GP, WZ><<<grid, block, 0, st>>>(Q, K, V, O, dO, LSE, Drow, TS, dQ, rho, \
                                                       msum, lambda, Z, s.BH, s.N, s.causal,  \
-                                                      s.scale)
+                                                      s.scale, s.G)
     if (s.d == 64) {
         if (mode == 2) GPA_DQ(64, true, true);
         else if (mode == 1) GPA_DQ(64, true, false);
@@ -659,20 +710,30 @@ hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V
 
 hipError_t launch_bwd_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                            const uint16_t* dO, const float* TS, const uint16_t* Z,
-                           uint16_t* dK, uint16_t* dV, int mode, const Shape& s,
-                           hipStream_t st) {
+                           uint16_t* dK, uint16_t* dV, float* dKp, float* dVp, int mode,
+                           const Shape& s, hipStream_t st) {
     const int T = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
     const bool gp = mode == 2;
 #define GPA_DKDV(DD, GP)                                                             \
-    bwd_dkdv_kernel<DD, GP><<<grid, block, 0, st>>>(Q, K, V, dO, TS, Z, dK, dV, s.BH, s.N, \
-                                                    s.causal, s.scale)
+    bwd_dkdv_kernel<DD, GP><<<grid, block, 0, st>>>(Q, K, V, dO, TS, Z, dK, dV, dKp, dVp, \
+                                                    s.BH, s.N, s.causal, s.scale, s.G)
     if (s.d == 64) {
         if (gp) GPA_DKDV(64, true); else GPA_DKDV(64, false);
     } else {
         if (gp) GPA_DKDV(128, true); else GPA_DKDV(128, false);
     }
 #undef GPA_DKDV
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_group_sum(const float* dKp, const float* dVp, uint16_t* dK, uint16_t* dV,
+                                const Shape& s, hipStream_t st) {
+    const int BHkv = s.BH / s.G;
+    const size_t per_head = (size_t)s.N * s.d;
+    const size_t threads = (size_t)BHkv * (per_head / 4);
+    dim3 grid((unsigned)((threads + 255) / 256)), block(256);
+    group_sum_kernel<<<grid, block, 0, st>>>(dKp, dVp, dK, dV, BHkv, s.G, per_head, s.scale);
     return hipGetLastError();
 }
 

@@ -27,7 +27,7 @@ template <int D>
 __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, uint16_t* __restrict__ O, float* __restrict__ LSE,
-    int BH, int N, int causal, float scale) {
+    int BH, int N, int causal, float scale, int G) {
     constexpr int MB = D / 16;
     constexpr int KC = D / 32;
     constexpr int PER_NB = MB * 4 + 2;  // acc, m, l of one query block
@@ -39,7 +39,8 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
     const int T = (N + kTile - 1) / kTile;
     int bh, tile;
     map_block(blockIdx.x, BH, T, causal != 0, &bh, &tile);
-    const size_t hoff = (size_t)bh * N * D;
+    const size_t hoff = (size_t)bh * N * D;        // query head: Q, O
+    const size_t kvoff = (size_t)(bh / G) * N * D;  // its key/value head
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -88,8 +89,8 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
 
     TileDma<D> dma;
     dma.init(lane, wave);
-    dma.load(K + hoff, KV0[0], 0, N);
-    dma.load(V + hoff, KV0[1], 0, N);
+    dma.load(K + kvoff, KV0[0], 0, N);
+    dma.load(V + kvoff, KV0[1], 0, N);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
@@ -98,8 +99,8 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
         constexpr bool MASK = decltype(masked)::value;
         const int k0 = kt * kTile;
         if (kt + 1 < nkv) {
-            dma.load(K + hoff, Kn, k0 + kTile, N);
-            dma.load(V + hoff, Vn, k0 + kTile, N);
+            dma.load(K + kvoff, Kn, k0 + kTile, N);
+            dma.load(V + kvoff, Vn, k0 + kTile, N);
         }
         // Keep the loads of the next tile at the top of the step: left alone,
         // the scheduler sinks them next to the closing wait, which exposes
@@ -243,9 +244,11 @@ hipError_t launch_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, u
     const int T = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
     if (s.d == 64)
-        fwd_sbs_kernel<64><<<grid, block, 0, st>>>(Q, K, V, O, LSE, s.BH, s.N, s.causal, s.scale);
+        fwd_sbs_kernel<64><<<grid, block, 0, st>>>(Q, K, V, O, LSE, s.BH, s.N, s.causal, s.scale,
+                                                   s.G);
     else
-        fwd_sbs_kernel<128><<<grid, block, 0, st>>>(Q, K, V, O, LSE, s.BH, s.N, s.causal, s.scale);
+        fwd_sbs_kernel<128><<<grid, block, 0, st>>>(Q, K, V, O, LSE, s.BH, s.N, s.causal, s.scale,
+                                                    s.G);
     return hipGetLastError();
 }
 

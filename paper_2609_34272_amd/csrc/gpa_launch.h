@@ -8,11 +8,13 @@
 namespace gpa {
 
 struct Shape {
-    int BH;        // batch * heads
+    int BH;        // batch * query heads
     int N;         // sequence length
     int d;         // head dimension (64 or 128)
     int causal;    // 1: key j visible to query i iff j <= i
     float scale;   // attention scale alpha
+    int G;         // query heads per key/value head (1: multi-head attention);
+                   // query head bh reads key/value head bh / G
 };
 
 // Kernel ids for timing (gpa_profile_*).
@@ -24,7 +26,8 @@ enum KernelId {
     kKF32Pre = 4,
     kKF32Dq = 5,
     kKF32Dkdv = 6,
-    kNumKernels = 7
+    kKGroupSum = 7,
+    kNumKernels = 8
 };
 
 hipError_t launch_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, uint16_t* O,
@@ -40,11 +43,19 @@ hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V
                          float* TS, uint16_t* dQ, float* rho, float* msum, float* lambda,
                          uint16_t* Z, int mode, const Shape& s, hipStream_t st);
 
-// Key-major pass: dV = r^T dO, dK = t^T Q (minus r^T Z in gproj mode).
+// Key-major pass: dV = r^T dO, dK = t^T Q (minus r^T Z in gproj mode).  With
+// G == 1 it writes BF16 dK, dV; with G > 1 every query head writes its FP32
+// contributions (dKp = t^T Q - r^T Z unscaled, dVp = r^T dO; [BH, N, d]) and
+// launch_bwd_group_sum adds them per key/value head.
 hipError_t launch_bwd_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                            const uint16_t* dO, const float* TS, const uint16_t* Z,
-                           uint16_t* dK, uint16_t* dV, int mode, const Shape& s,
-                           hipStream_t st);
+                           uint16_t* dK, uint16_t* dV, float* dKp, float* dVp, int mode,
+                           const Shape& s, hipStream_t st);
+
+// dK = BF16(scale * sum_g dKp), dV = BF16(sum_g dVp) over the G query heads of
+// each key/value head, in head order.
+hipError_t launch_bwd_group_sum(const float* dKp, const float* dVp, uint16_t* dK, uint16_t* dV,
+                                const Shape& s, hipStream_t st);
 
 // FP32 baseline.
 hipError_t launch_f32_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, float* O32,

@@ -18,6 +18,10 @@ Recipe for one (batch b, head h) of a workload with seed s:
   every tensor is rounded to FP32 (round-to-nearest-even) and then to BF16
   (round-to-nearest-even).
 Per-head seeding lets any subset of heads be regenerated on its own.
+
+Grouped-query workloads (Hkv < H) draw every query head as above and give key/value
+head j the K and V drawn for query head j*G (G = H / Hkv), the first head of
+its group; the other heads' K, V draws are discarded.
 """
 from __future__ import annotations
 
@@ -49,6 +53,11 @@ class Workload:
     q_bias_std: float = 0.0
     k_bias_std: float = 0.0
     do_std: float = 1.0
+    Hkv: int | None = None  # key/value heads (None: H, multi-head attention)
+
+    @property
+    def kv_heads(self) -> int:
+        return self.H if self.Hkv is None else self.Hkv
 
     @property
     def scale(self) -> float:
@@ -66,6 +75,8 @@ WORKLOADS = {
                 do_std=0.01),
     4: Workload("h16_n16384_d64", 1, 16, 16384, 64, k_bias_std=8.0, do_std=0.01),
     5: Workload("b8_h32_n8192_d128", 8, 32, 8192, 128, k_bias_std=4.0, do_std=0.01),
+    # The paper's capture layout: 16 query heads sharing 4 key/value heads.
+    6: Workload("gqa_h16kv4_n4096_d64", 1, 16, 4096, 64, k_bias_std=4.0, do_std=0.01, Hkv=4),
 }
 
 
@@ -114,24 +125,35 @@ def make_head(w: Workload, seed: int, b: int, h: int, N: int | None = None):
 
 
 def make_inputs(w: Workload, seed: int, heads=None):
-    """Generate a workload as uint16 BF16 bit arrays shaped [B, H, N, d].
+    """Generate a workload as uint16 BF16 bit arrays: q, do [B, H, N, d] and
+    k, v [B, Hkv, N, d].
 
-    heads: optional list of (b, h) pairs; if given, the arrays are shaped
-    [len(heads), 1, N, d] holding only those heads (same values as in the
-    full tensor).
+    heads: optional list of (b, h) pairs (multi-head workloads only); if given,
+    the arrays are shaped [len(heads), 1, N, d] holding only those heads (same
+    values as in the full tensor).
     """
+    Hkv = w.kv_heads
+    if heads is not None and Hkv != w.H:
+        raise ValueError("head subsets are for multi-head workloads")
     if heads is None:
         pairs = [(b, h) for b in range(w.B) for h in range(w.H)]
         shape = (w.B, w.H, w.N, w.d)
+        kv_shape = (w.B, Hkv, w.N, w.d)
     else:
         pairs = list(heads)
-        shape = (len(pairs), 1, w.N, w.d)
-    out = {n: np.empty(shape, dtype=np.uint16) for n in ("q", "k", "v", "do")}
+        shape = kv_shape = (len(pairs), 1, w.N, w.d)
+    G = w.H // Hkv
+    out = {n: np.empty(shape, dtype=np.uint16) for n in ("q", "do")}
+    out.update({n: np.empty(kv_shape, dtype=np.uint16) for n in ("k", "v")})
     for idx, (b, h) in enumerate(pairs):
         q, k, v, u = make_head(w, seed, b, h)
         bi, hi = divmod(idx, shape[1])
         out["q"][bi, hi] = q
-        out["k"][bi, hi] = k
-        out["v"][bi, hi] = v
         out["do"][bi, hi] = u
+        if heads is not None:
+            out["k"][bi, hi] = k
+            out["v"][bi, hi] = v
+        elif hi % G == 0:
+            out["k"][bi, hi // G] = k
+            out["v"][bi, hi // G] = v
     return out

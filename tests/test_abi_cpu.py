@@ -107,3 +107,17 @@ def test_python_binding_rejects_cpu_tensors():
     q = torch.zeros(1, 1, 8, 64, dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         gpa.attn_fwd(q, q, q)
+
+
+def test_gqa_validation(lib):
+    P = FAKE
+    # Hq not a multiple of Hkv
+    assert lib.gpa_attn_fwd_gqa(P, P + 0x10000000, P + 0x20000000, P + 0x30000000, P + 0x40000000,
+                                1, 6, 4, 128, 64, 1, 0.125, None) == 1
+    assert b"multiple" in lib.gpa_last_error()
+    assert lib.gpa_attn_bwd_gqa_workspace_bytes(1, 6, 4, 128, 64, 2) == 0
+    # grouped workspace adds the per-head FP32 contributions
+    mha = lib.gpa_attn_bwd_gqa_workspace_bytes(1, 16, 16, 4096, 64, 2)
+    gqa = lib.gpa_attn_bwd_gqa_workspace_bytes(1, 16, 4, 4096, 64, 2)
+    assert mha == lib.gpa_attn_bwd_workspace_bytes(1, 16, 4096, 64, 2)
+    assert gqa == mha + 2 * 16 * 4096 * 64 * 4

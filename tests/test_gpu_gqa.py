@@ -1,0 +1,128 @@
+"""Grouped-query attention through the C ABI (gpa_attn_fwd_gqa /
+gpa_attn_bwd_gqa) against the CPU oracle.
+
+Query head h reads key/value head h // G.  Per query head the forward and the
+query-major pass are exactly the multi-head ones, so O, LSE and dQ must equal
+the multi-head results on K, V repeated G times bit for bit; dK and dV sum the
+group's per-head FP32 contributions, so they are checked against the exact
+FP64 grouped VJP with the accuracy gates of the multi-head tests (gproj within
+1.0 % and within 2x an FP32 attention baseline; plain blows up on biased keys).
+The FP32 baseline for a group is the multi-head FP32 attention on repeated K,
+V with its per-head dK, dV added on the host.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synthetic as S
+
+import _gpu as G
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU"),
+              pytest.mark.filterwarnings("ignore::RuntimeWarning")]
+
+MODES = ("plain", "gproj_q", "gproj")
+NAMES = ("dQ", "dK", "dV")
+
+
+@pytest.fixture(scope="module")
+def gpa():
+    import paper_2609_34272_amd as gpa
+    gpa.lib()
+    return gpa
+
+
+def run_gqa(gpa, x, causal, scale):
+    q, k, v, u = (G.to_dev(x[n]) for n in ("q", "k", "v", "do"))
+    o, lse = gpa.attn_fwd(q, k, v, causal, scale)
+    out = {"O": o, "LSE": lse}
+    for m in MODES:
+        dq, dk, dv, st = gpa.attn_bwd(q, k, v, o, lse, u, m, causal, scale, return_stats=True)
+        out[m] = dict(dQ=dq, dK=dk, dV=dv, stats={n: t.clone() for n, t in st.items()})
+    torch.cuda.synchronize()
+    return out
+
+
+def run_repeated(gpa, x, G_, causal, scale, fp32=True):
+    """Multi-head runs on K, V repeated over each group."""
+    q, u = G.to_dev(x["q"]), G.to_dev(x["do"])
+    k = G.to_dev(np.repeat(x["k"], G_, axis=1))
+    v = G.to_dev(np.repeat(x["v"], G_, axis=1))
+    o, lse = gpa.attn_fwd(q, k, v, causal, scale)
+    out = {"O": o, "LSE": lse}
+    for m in MODES:
+        dq, dk, dv = gpa.attn_bwd(q, k, v, o, lse, u, m, causal, scale)
+        out[m] = dict(dQ=dq, dK=dk, dV=dv)
+    if fp32:
+        fo, flse, fdq, fdk, fdv = gpa.fp32_attn(q, k, v, u, causal, scale)
+        B, Hq, N, d = x["q"].shape
+        grp = lambda t: G.to_host(t).reshape(B, Hq // G_, G_, N, d).sum(axis=2)  # noqa: E731
+        out["fp32"] = dict(O=G.to_host(fo), dQ=G.to_host(fdq), dK=grp(fdk), dV=grp(fdv))
+    torch.cuda.synchronize()
+    return out
+
+
+def check(gpa, x, causal, scale, tag, blowup_ratio=3.0):
+    B, Hq, N, d = x["q"].shape
+    G_ = Hq // x["k"].shape[1]
+    out = run_gqa(gpa, x, causal, scale)
+    rep = run_repeated(gpa, x, G_, causal, scale)
+    # per query head: bitwise the multi-head results
+    assert np.array_equal(G.bits(out["O"]), G.bits(rep["O"])), tag
+    assert torch.equal(out["LSE"], rep["LSE"]), tag
+    for m in MODES:
+        assert np.array_equal(G.bits(out[m]["dQ"]), G.bits(rep[m]["dQ"])), (tag, m)
+    # mode identities hold through the group sum
+    b = lambda m, n: G.bits(out[m][n])  # noqa: E731
+    assert np.array_equal(b("plain", "dK"), b("gproj_q", "dK"))
+    assert np.array_equal(b("plain", "dV"), b("gproj_q", "dV"))
+    assert np.array_equal(b("gproj_q", "dV"), b("gproj", "dV"))
+    ex = oracle.exact(x["q"], x["k"], x["v"], x["do"], causal, scale)
+    e = {m: {n: G.rel_l2(G.to_host(out[m][n]), ex[n]) for n in NAMES} for m in MODES}
+    e["fp32"] = {n: G.rel_l2(rep["fp32"][n], ex[n]) for n in NAMES}
+    eo = G.rel_l2(G.to_host(out["O"]), ex["O"])
+    G.log(f"[{tag}] O {eo:.4f}% | " + " | ".join(
+        f"{m}: " + "/".join(f"{e[m][n]:.4f}" for n in NAMES) for m in MODES + ("fp32",)))
+    assert eo <= 0.5
+    for n in NAMES:
+        assert e["gproj"][n] <= 1.0, (tag, n, e["gproj"][n])
+        assert e["gproj"][n] <= 2.0 * e["fp32"][n], (tag, "vs fp32", n)
+    if blowup_ratio:
+        assert e["plain"]["dQ"] >= blowup_ratio * e["gproj"]["dQ"], (tag, "no blow-up")
+    return out
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,N,d,causal", [
+    (1, 4, 1, 128, 64, True), (1, 4, 2, 200, 64, True), (2, 6, 3, 129, 128, True),
+    (1, 8, 2, 65, 64, False), (1, 2, 1, 1, 64, True)])
+def test_gqa_small(gpa, B, Hq, Hkv, N, d, causal):
+    w = S.Workload("gqa", B, Hq, N, d, causal=causal, k_bias_std=8.0, do_std=1.0, Hkv=Hkv)
+    x = S.make_inputs(w, 500 + N)
+    tag = f"gqa {B}x{Hq}/{Hkv}x{N}x{d} causal={causal}"
+    if N == 1:
+        # singleton rows: exact dQ = dK = 0; GProj's dQ is exactly zero, the
+        # other modes keep only the cast leak of size ~ eps * |k|
+        out = run_gqa(gpa, x, causal, w.scale)
+        kmax = np.abs(S.bf16_bits_to_f32(x["k"])).max()
+        assert np.abs(G.to_host(out["gproj"]["dQ"])).max() == 0.0
+        for m in MODES:
+            assert np.abs(G.to_host(out[m]["dQ"])).max() <= 1e-6 * max(1.0, kmax)
+            assert np.abs(G.to_host(out[m]["dK"])).max() <= 1e-6 * max(1.0, kmax)
+        assert np.array_equal(G.bits(out["O"]), np.repeat(x["v"], Hq // Hkv, axis=1))
+        return
+    check(gpa, x, causal, w.scale, tag, blowup_ratio=3.0 if (causal and N >= 128) else 0)
+
+
+def test_gqa_capture_layout_h16_kv4(gpa):
+    """The paper's capture layout (16 query heads, 4 key/value heads, N = 4096,
+    d = 64, scale 1/8) on synthetic biased-key inputs; also bitwise
+    reproducible."""
+    w = S.WORKLOADS[6]
+    x = S.make_inputs(w, 6000)
+    out = check(gpa, x, w.causal, w.scale, "gqa_h16kv4_n4096_d64")
+    again = run_gqa(gpa, x, w.causal, w.scale)
+    for m in MODES:
+        for n in NAMES:
+            assert np.array_equal(G.bits(out[m][n]), G.bits(again[m][n])), (m, n)

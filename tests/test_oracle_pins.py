@@ -257,3 +257,58 @@ def test_rel_l2_metric():
     t = np.array([3.0, 4.0])
     assert oracle.rel_l2(t * 1.01, t) == pytest.approx(1.0)
     assert oracle.rel_l2(t, t) == 0.0
+
+
+# ------------------------------------------------------ grouped-query attention
+
+def test_gqa_decimal_directional_derivative():
+    """Grouped-query attention: L = sum over query heads of sum(O_h * dO_h) with
+    the key/value head shared.  Its directional derivative from the 50-digit
+    brute force equals <grad, direction> from the oracle, which pins the sum of
+    every query head's contribution into the shared dK, dV (Section 3.2)."""
+    rng = np.random.default_rng(21)
+    Hq, N, d, alpha = 3, 4, 3, 0.8
+    q = rng.standard_normal((Hq, N, d))
+    k = rng.standard_normal((N, d)) + 1.5 * rng.standard_normal(d)[None, :]
+    v = rng.standard_normal((N, d))
+    u = rng.standard_normal((Hq, N, d))
+    ex = oracle.exact(q[None], k[None, None], v[None, None], u[None], True, alpha)
+    dq_dir = rng.standard_normal((Hq, N, d))
+    dk_dir, dv_dir = rng.standard_normal((N, d)), rng.standard_normal((N, d))
+    h = decimal.Decimal("1e-15")
+    Lp = Lm = decimal.Decimal(0)
+    for hh in range(Hq):
+        dirs = (dq_dir[hh], dk_dir, dv_dir)
+        Lp += _decimal_forward(q[hh], k, v, u[hh], True, alpha, dirs=dirs, h=h)[2]
+        Lm += _decimal_forward(q[hh], k, v, u[hh], True, alpha, dirs=dirs, h=-h)[2]
+    fd = float((Lp - Lm) / (2 * h))
+    an = float(np.sum(ex["dQ"][0] * dq_dir) + np.sum(ex["dK"][0, 0] * dk_dir)
+               + np.sum(ex["dV"][0, 0] * dv_dir))
+    # FP64 rounding over three heads stays near 1e-12; a dropped head or a
+    # wrong key/value head would be off by O(0.1).
+    assert abs(fd - an) <= 1e-11 * max(1.0, abs(an))
+
+
+def test_gqa_conservation_and_per_head_identity():
+    """Per key/value head, sum_j dk_j = 0 (each query head's rows of dS sum to
+    zero) and sum_j dv_j = sum over its query heads and rows of dO; each query
+    head's O, LSE, dQ are those of multi-head attention against the shared K, V."""
+    rng = np.random.default_rng(8)
+    B, Hq, Hkv, N, d = 2, 4, 2, 11, 4
+    q = rng.standard_normal((B, Hq, N, d))
+    k = rng.standard_normal((B, Hkv, N, d)) + 3.0
+    v = rng.standard_normal((B, Hkv, N, d))
+    u = rng.standard_normal((B, Hq, N, d))
+    for causal in (True, False):
+        ex = oracle.exact(q, k, v, u, causal, 0.6)
+        G = Hq // Hkv
+        for b in range(B):
+            for j in range(Hkv):
+                assert np.abs(ex["dK"][b, j].sum(axis=0)).max() < 1e-12 * (1 + np.abs(ex["dK"][b, j]).max())
+                want = u[b, j * G:(j + 1) * G].sum(axis=(0, 1))
+                assert np.allclose(ex["dV"][b, j].sum(axis=0), want, rtol=0, atol=1e-12)
+                for g in range(G):
+                    h = j * G + g
+                    one = _exact_head(q[b, h], k[b, j], v[b, j], u[b, h], causal, 0.6)
+                    for n in ("O", "LSE", "dQ"):
+                        assert np.array_equal(ex[n][b, h], one[n])
