@@ -293,6 +293,9 @@ __device__ __forceinline__ void map_block(int bid, int BH, int T, bool heavy_hig
 #ifndef GPA_FWD_OCC
 #define GPA_FWD_OCC 2
 #endif
+#ifndef GPA_FWD16_OCC
+#define GPA_FWD16_OCC 4
+#endif
 #ifndef GPA_DQ_OCC64
 #define GPA_DQ_OCC64 2
 #endif

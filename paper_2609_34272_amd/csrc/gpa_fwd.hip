@@ -237,15 +237,163 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
     }
 }
 
+// Variant with one 16-query block per wave: each of the 4 waves owns 16 of
+// the workgroup's 64 queries and runs them against the whole 64-key tile, so
+// the online-softmax bookkeeping (row maximum, rescale of the output
+// accumulator, correction factor) is paid once per 64 keys and no merge of
+// partial states is needed; the price is that every K and V fragment read from
+// LDS feeds one MFMA instead of two.  Fewer registers per wave allow more
+// waves per SIMD.  The arithmetic per (query, key) is that of fwd_sbs_kernel.
+template <int D>
+__global__ __launch_bounds__(kThreads, GPA_FWD16_OCC) void fwd_sbs_q16_kernel(
+    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
+    const uint16_t* __restrict__ V, uint16_t* __restrict__ O, float* __restrict__ LSE,
+    int BH, int N, int causal, float scale, int G) {
+    constexpr int MB = D / 16;
+    constexpr int KC = D / 32;
+    __shared__ __attribute__((aligned(16))) uint16_t KV0[2][kTile * D];
+    __shared__ __attribute__((aligned(16))) uint16_t KV1[2][kTile * D];
+
+    const int T = (N + kTile - 1) / kTile;
+    int bh, tile;
+    map_block(blockIdx.x, BH, T, causal != 0, &bh, &tile);
+    const size_t hoff = (size_t)bh * N * D;
+    const size_t kvoff = (size_t)(bh / G) * N * D;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, c16 = lane & 15;
+    const int qrow = tile * kTile + 16 * wave + c16;  // this lane's query
+
+    const rsrc_t rq = make_rsrc(Q + hoff, (uint32_t)N * (2 * D));
+    bf16x8 qf[KC];
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc)
+        qf[kc] = __builtin_bit_cast(bf16x8, ld_row16<D>(rq, qrow, kc * 32 + 8 * g));
+
+    const float c = scale * kLog2e;
+    float mrun = -INFINITY, lrun = 0.f;
+    f32x4 acc[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int kv_end = causal ? min(N, (tile + 1) * kTile) : N;
+    const int nkv = (kv_end + kTile - 1) / kTile;
+    const int nplain = (causal || (N % kTile)) ? nkv - 1 : nkv;
+
+    TileDma<D> dma;
+    dma.init(lane, wave);
+    wait_vm_lgkm0<0>();
+    dma.load(K + kvoff, KV0[0], 0, N);
+    dma.load(V + kvoff, KV0[1], 0, N);
+    wait_vm_lgkm0<0>();
+    __builtin_amdgcn_s_barrier();
+
+    auto step = [&](auto masked, int kt, const uint16_t* Kc, const uint16_t* Vc, uint16_t* Kn,
+                    uint16_t* Vn) {
+        constexpr bool MASK = decltype(masked)::value;
+        const int k0 = kt * kTile;
+        if (kt + 1 < nkv) {
+            dma.load(K + kvoff, Kn, k0 + kTile, N);
+            dma.load(V + kvoff, Vn, k0 + kTile, N);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        // S^T[key][query]: s[kb] holds keys 16 kb + 4g + i for this lane's query.
+        f32x4 s[4];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+            s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kc = 0; kc < KC; ++kc)
+                s[kb] = mfma_16x16x32(ld_b128(Kc + tile_off<D>(kb * 16 + c16, kc * 32 + 8 * g)),
+                                      qf[kc], s[kb]);
+        }
+        if constexpr (MASK) {
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int key = k0 + kb * 16 + 4 * g + i;
+                    const bool ok = key < N && (!causal || key <= qrow);
+                    s[kb][i] = ok ? s[kb][i] : -INFINITY;
+                }
+        }
+        float mx = s[0][0];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[kb][i]);
+        mx = xor_max(mx);
+        const float mnew = fmaxf(mrun, mx);
+        const float ms = (mnew == -INFINITY) ? 0.f : mnew;
+        const float corr = fexp2((mrun - ms) * c);
+        lrun *= corr;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) acc[mb] *= corr;
+        // pf[j]: B operand of keys 32 j .. 32 j + 31 (k-layout {4g+i, 16+4g+i}).
+        bf16x8 pf[2];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float z = fexp2((s[kb][i] - ms) * c);
+                lrun += z;
+                pf[kb >> 1][(kb & 1) * 4 + i] = to_bf16(z);
+            }
+        mrun = mnew;
+        // O^T[dv][query] += V^T[dv][key] P^T[key][query].
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                acc[mb] = mfma_16x16x32(ld_tr_operand<D>(Vc, 32 * j, mb * 16, c16, g), pf[j],
+                                        acc[mb]);
+        wait_vm_lgkm0<0>();
+        __builtin_amdgcn_s_barrier();
+    };
+    const std::false_type plain;
+    const std::true_type masked;
+    int kt = 0;
+    for (; kt + 1 < nplain; kt += 2) {
+        step(plain, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
+        step(plain, kt + 1, KV1[0], KV1[1], KV0[0], KV0[1]);
+    }
+    if (kt < nplain) {
+        step(plain, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
+        if (kt + 1 < nkv) step(masked, kt + 1, KV1[0], KV1[1], KV0[0], KV0[1]);
+    } else if (kt < nkv) {
+        step(masked, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
+    }
+
+    const float ltot = xor_sum(lrun);
+    if (qrow < N) {
+        uint16_t* orow = O + hoff + (size_t)qrow * D;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            float v[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] = acc[mb][i] / ltot;
+            st_bf16x4(orow + mb * 16 + 4 * g, v[0], v[1], v[2], v[3]);
+        }
+        if (g == 0) {
+#pragma clang fp contract(off)
+            const float lse = scale * mrun + logf(ltot);
+            LSE[(size_t)bh * N + qrow] = lse;
+        }
+    }
+}
+
 }  // namespace
 
 hipError_t launch_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, uint16_t* O,
                       float* LSE, const Shape& s, hipStream_t st) {
     const int T = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
+    // d = 64: one 16-query block per wave (measured faster); d = 128: two
+    // blocks per wave, whose halved LDS reads matter more there.
     if (s.d == 64)
-        fwd_sbs_kernel<64><<<grid, block, 0, st>>>(Q, K, V, O, LSE, s.BH, s.N, s.causal, s.scale,
-                                                   s.G);
+        fwd_sbs_q16_kernel<64><<<grid, block, 0, st>>>(Q, K, V, O, LSE, s.BH, s.N, s.causal,
+                                                       s.scale, s.G);
     else
         fwd_sbs_kernel<128><<<grid, block, 0, st>>>(Q, K, V, O, LSE, s.BH, s.N, s.causal, s.scale,
                                                     s.G);
