@@ -37,8 +37,10 @@ def parse():
     p.add_argument("--mode", default="gproj", choices=["plain", "gproj_q", "gproj"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-accuracy", action="store_true")
+    p.add_argument("--no-gqa", action="store_true",
+                   help="skip the timing of the grouped-query layout (16 query / 4 key-value heads)")
     p.add_argument("--calibrate-copy", action="store_true",
-                   help="also run a plain 64 MiB device copy (reference for HBM byte counters)")
+                   help="also run a cache-cold 512 MiB device copy (reference for HBM byte counters)")
     return p.parse_args()
 
 
@@ -140,6 +142,29 @@ def main():
                                                workspace=ws[m]), args.steps)
     fwd_ms = timed(lambda: gpa.attn_fwd(q, k, v, w.causal, w.scale), args.steps)
 
+    # Context: the paper's grouped-query capture layout (16 query heads sharing
+    # 4 key/value heads, same N, d and input recipe), forward and backward alone.
+    gqa = None
+    if not args.no_gqa:
+        wg = S.WORKLOADS[6]
+        xg = S.make_inputs(wg, 6000)
+        qg, kg, vg, ug = (to_dev(xg[n]) for n in ("q", "k", "v", "do"))
+        og, lg = gpa.attn_fwd(qg, kg, vg, wg.causal, wg.scale)
+        gqa = {"workload": wg.name, "Hq": wg.H, "Hkv": wg.kv_heads,
+               "fwd_ms": round(timed(lambda: gpa.attn_fwd(qg, kg, vg, wg.causal, wg.scale),
+                                     args.steps), 5), "bwd_ms": {}}
+        for m in gpa.MODES:
+            wsg = torch.empty(gpa.attn_bwd_workspace_bytes(wg.B, wg.H, wg.N, wg.d, m, wg.kv_heads),
+                              dtype=torch.uint8, device=dev)
+            fn = lambda: gpa.attn_bwd(qg, kg, vg, og, lg, ug, m, wg.causal, wg.scale,  # noqa: E731
+                                      workspace=wsg)
+            for _ in range(3):
+                fn()
+            gqa["bwd_ms"][m] = round(timed(fn, args.steps), 5)
+        gqa["gproj_bwd_overhead_vs_plain_pct"] = round(
+            100.0 * (gqa["bwd_ms"]["gproj"] / gqa["bwd_ms"]["plain"] - 1), 2)
+        del qg, kg, vg, ug, og, lg
+
     # Roofline of the dominant kernel: algorithmic MFMA flops per launch.
     pairs = B * H * N * N / 2.0
     # dense contractions each kernel needs for its own outputs (per causal pair, 2d flops each):
@@ -172,6 +197,8 @@ def main():
         "gproj_q_bwd_overhead_vs_plain_pct": round(100.0 * (bwd_ms["gproj_q"] / bwd_ms["plain"] - 1), 2),
         "wall_s_timed": round(wall, 3),
     }
+    if gqa is not None:
+        out["gqa"] = gqa
 
     if not args.no_accuracy or not args.no_cpu_baseline:
         import oracle
