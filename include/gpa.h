@@ -134,6 +134,21 @@ gpa_status gpa_bwd_stats_offsets(int64_t B, int64_t H, int64_t N, int64_t d, int
                                  size_t* off_lambda);
 
 /*
+ * Diagnostic forward, not part of the GProj path: gpa_attn_fwd with the
+ * historical exponent rounding r = fma(x, a, -fl32(m a)), z = exp2(r), a =
+ * fl32(scale log2 e), m the running row maximum (appendix on the source of the
+ * saved-output error, eq. historical-fma), everything else as gpa_attn_fwd.
+ * Because r is the rounding error of x a instead of 0 when x = m, a row with a
+ * single visible key can return BF16(BF16(z) v / z) != v (eq.
+ * historical-one-key).  Multi-head only; same arguments and errors as
+ * gpa_attn_fwd.
+ */
+gpa_status gpa_attn_fwd_fma(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                            uint16_t* O, float* LSE,
+                            int64_t B, int64_t H, int64_t N, int64_t d,
+                            int causal, float scale, void* stream);
+
+/*
  * Grouped-query attention (Section 3.2, eq. row-gradients: key and value
  * gradients also sum over the query heads that share a KV head; appendix
  * "Gauge Projection: Proofs", "Rounding in the implemented key correction":

@@ -179,3 +179,28 @@ def project_query_row(t, r, K, alpha):
     m = r.sum()
     lam = rho / m if m != 0 else 0.0
     return alpha * (t @ K - lam * (r @ K))
+
+
+# ------------------------------------------------------------------ diagnostic
+def historical_fma_one_key(x, alpha, v):
+    """Output row of a query with exactly one visible key under the historical
+    FMA forward (appendix on the source of the saved-output error, eqs.
+    historical-fma and historical-one-key), the scalar model the paper uses to
+    explain the one-key violations:
+        a = fl32(alpha log2 e),  r = fma(x, a, -fl32(x a)),  z = exp2_32(r),
+        o = BF16( fl32[ BF16(z) v / z ] )
+    x is the (FP32) unscaled logit of the single key, which is also the row
+    maximum; v the key's value row (BF16 values).  The FMA rounds the exact
+    x*a - fl32(x a) once to FP32 (computed exactly in FP64: the product of two
+    FP32 values has at most 48 significant bits, and the difference is the
+    rounding error of that product, exactly representable).  Returns float32.
+    """
+    a = np.float32(np.float32(alpha) * np.float32(LOG2E))
+    x32 = np.float32(x)
+    ma = np.float32(x32 * a)                           # fl32(m a)
+    exact = np.float64(x32) * np.float64(a) - np.float64(ma)
+    r = np.float32(exact)                              # the FMA's single rounding
+    z = np.exp2(r, dtype=np.float32)
+    zb = bf16_round(np.float32(z))
+    acc = (np.asarray(v, dtype=np.float32) * np.float32(zb)).astype(np.float32)
+    return bf16_round((acc / np.float32(z)).astype(np.float32))

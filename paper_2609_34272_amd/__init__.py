@@ -25,7 +25,7 @@ import os
 import torch  # noqa: F401  (load torch's HIP runtime first; libgpa binds to it)
 
 __all__ = [
-    "MODES", "lib", "attn_fwd", "attn_bwd", "attn_bwd_workspace_bytes", "bwd_stats_offsets",
+    "MODES", "lib", "attn_fwd", "attn_fwd_fma", "attn_bwd", "attn_bwd_workspace_bytes", "bwd_stats_offsets",
     "fp32_attn", "fp32_attn_workspace_bytes", "profile_enable", "profile_read", "GpaError",
     "LIB_PATH",
 ]
@@ -65,6 +65,8 @@ def lib():
     L.gpa_attn_bwd_workspace_bytes.argtypes = [I64, I64, I64, I64, INT]
     L.gpa_attn_bwd.restype = INT
     L.gpa_attn_bwd.argtypes = [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, INT, F32, INT, P, SZ, P]
+    L.gpa_attn_fwd_fma.restype = INT
+    L.gpa_attn_fwd_fma.argtypes = [P, P, P, P, P, I64, I64, I64, I64, INT, F32, P]
     L.gpa_attn_fwd_gqa.restype = INT
     L.gpa_attn_fwd_gqa.argtypes = [P, P, P, P, P, I64, I64, I64, I64, I64, INT, F32, P]
     L.gpa_attn_bwd_gqa_workspace_bytes.restype = SZ
@@ -147,6 +149,20 @@ def attn_fwd(q, k, v, causal: bool = True, scale=None):
         _check(lib().gpa_attn_fwd_gqa(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
                                       lse.data_ptr(), B, H, Hkv, N, d, int(bool(causal)),
                                       _scale(d, scale), _stream(q)))
+    return o, lse
+
+
+def attn_fwd_fma(q, k, v, causal: bool = True, scale=None):
+    """Diagnostic forward with the historical FMA exponent rounding (not the
+    GProj path).  Multi-head only.  Returns O, LSE like attn_fwd."""
+    B, H, N, d = _shape(q)
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _need(t, n, (B, H, N, d), torch.bfloat16)
+    o = torch.empty_like(q)
+    lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    _check(lib().gpa_attn_fwd_fma(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                  lse.data_ptr(), B, H, N, d, int(bool(causal)), _scale(d, scale),
+                                  _stream(q)))
     return o, lse
 
 

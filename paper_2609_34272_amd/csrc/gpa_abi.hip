@@ -185,6 +185,21 @@ gpa_status gpa_attn_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
     return gpa_attn_fwd_gqa(Q, K, V, O, LSE, B, H, H, N, d, causal, scale, stream);
 }
 
+gpa_status gpa_attn_fwd_fma(const uint16_t* Q, const uint16_t* K, const uint16_t* V, uint16_t* O,
+                            float* LSE, int64_t B, int64_t H, int64_t N, int64_t d, int causal,
+                            float scale, void* stream) {
+    gpa_status s = check_shape(B, H, N, d, scale);
+    if (s != GPA_OK) return s;
+    const size_t tb = (size_t)B * H * N * d * 2, lb = (size_t)B * H * N * 4;
+    s = check_ptrs({{Q, tb, "Q"}, {K, tb, "K"}, {V, tb, "V"}}, {{O, tb, "O"}, {LSE, lb, "LSE"}});
+    if (s != GPA_OK) return s;
+    const gpa::Shape sh{(int)(B * H), (int)N, (int)d, causal ? 1 : 0, scale, 1};
+    hipStream_t st = (hipStream_t)stream;
+    return launched(
+        timed(gpa::kKFwd, st, [&] { return gpa::launch_fwd(Q, K, V, O, LSE, sh, st, true); }),
+        "fwd_fma");
+}
+
 size_t gpa_attn_bwd_gqa_workspace_bytes(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t d,
                                         int mode) {
     if (mode < 0 || mode > 2) return 0;

@@ -23,7 +23,24 @@
 namespace gpa {
 namespace {
 
-template <int D>
+// Exponent argument of z = exp2(arg).  FA3-SBS (the path's forward):
+// fl32[fl32(x - m) * c].  FMA (diagnostic only): the historical rounding
+// fma(x, c, -fl32(m * c)), whose result is the rounding error of x*c rather
+// than 0 when x = m (appendix on the source of the saved-output error, eq.
+// historical-fma).
+template <bool FMA>
+__device__ __forceinline__ float exp_arg(float x, float m, float c) {
+    if constexpr (FMA) {
+#pragma clang fp contract(off)
+        const float mc = m * c;
+        return __builtin_fmaf(x, c, -mc);
+    } else {
+#pragma clang fp contract(off)
+        return (x - m) * c;
+    }
+}
+
+template <int D, bool FMA>
 __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, uint16_t* __restrict__ O, float* __restrict__ LSE,
@@ -155,7 +172,7 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const float z = fexp2((s[nb][kb][i] - ms) * c);
+                    const float z = fexp2(exp_arg<FMA>(s[nb][kb][i], ms, c));
                     lrun[nb] += z;
                     pf[nb][kb * 4 + i] = to_bf16(z);
                 }
@@ -244,7 +261,7 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
 // partial states is needed; the price is that every K and V fragment read from
 // LDS feeds one MFMA instead of two.  Fewer registers per wave allow more
 // waves per SIMD.  The arithmetic per (query, key) is that of fwd_sbs_kernel.
-template <int D>
+template <int D, bool FMA>
 __global__ __launch_bounds__(kThreads, GPA_FWD16_OCC) void fwd_sbs_q16_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, uint16_t* __restrict__ O, float* __restrict__ LSE,
@@ -336,7 +353,7 @@ __global__ __launch_bounds__(kThreads, GPA_FWD16_OCC) void fwd_sbs_q16_kernel(
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const float z = fexp2((s[kb][i] - ms) * c);
+                const float z = fexp2(exp_arg<FMA>(s[kb][i], ms, c));
                 lrun += z;
                 pf[kb >> 1][(kb & 1) * 4 + i] = to_bf16(z);
             }
@@ -386,17 +403,21 @@ __global__ __launch_bounds__(kThreads, GPA_FWD16_OCC) void fwd_sbs_q16_kernel(
 }  // namespace
 
 hipError_t launch_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, uint16_t* O,
-                      float* LSE, const Shape& s, hipStream_t st) {
+                      float* LSE, const Shape& s, hipStream_t st, bool fma_forward) {
     const int T = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
     // d = 64: one 16-query block per wave (measured faster); d = 128: two
     // blocks per wave, whose halved LDS reads matter more there.
-    if (s.d == 64)
-        fwd_sbs_q16_kernel<64><<<grid, block, 0, st>>>(Q, K, V, O, LSE, s.BH, s.N, s.causal,
-                                                       s.scale, s.G);
-    else
-        fwd_sbs_kernel<128><<<grid, block, 0, st>>>(Q, K, V, O, LSE, s.BH, s.N, s.causal, s.scale,
-                                                    s.G);
+#define GPA_FWD(KERNEL, DD, FM)                                                               \
+    KERNEL<DD, FM><<<grid, block, 0, st>>>(Q, K, V, O, LSE, s.BH, s.N, s.causal, s.scale, s.G)
+    if (s.d == 64) {
+        if (fma_forward) GPA_FWD(fwd_sbs_q16_kernel, 64, true);
+        else GPA_FWD(fwd_sbs_q16_kernel, 64, false);
+    } else {
+        if (fma_forward) GPA_FWD(fwd_sbs_kernel, 128, true);
+        else GPA_FWD(fwd_sbs_kernel, 128, false);
+    }
+#undef GPA_FWD
     return hipGetLastError();
 }
 

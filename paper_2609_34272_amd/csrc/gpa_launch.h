@@ -30,8 +30,9 @@ enum KernelId {
     kNumKernels = 8
 };
 
+// fma_forward selects the historical exponent rounding (diagnostic only).
 hipError_t launch_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, uint16_t* O,
-                      float* LSE, const Shape& s, hipStream_t st);
+                      float* LSE, const Shape& s, hipStream_t st, bool fma_forward = false);
 
 // Query-major pass: writes D = rowsum(dO * O) and dQ; in the gproj modes also
 // rho, m, lambda (zero in plain mode); in gproj mode also Z = BF16(lambda Q)

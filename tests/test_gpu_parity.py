@@ -137,6 +137,37 @@ def test_single_key_rows(gpa):
                     assert np.abs(G.to_host(dq)[0, 0, 0]).max() == 0.0, (N, cval, kexp, m)
 
 
+def test_historical_fma_forward_one_key_rows(gpa):
+    """Diagnostic (not the GProj path): the historical FMA exponent rounding
+    (eq. historical-fma) on the same 96 single-key constructions.  The first
+    row's output must equal the paper's scalar model BF16(BF16(z) v / z) (eq.
+    historical-one-key) bit for bit in every case, some cases must violate
+    o0 = v0, and the FA3-SBS forward on the same inputs must not."""
+    rng = np.random.default_rng(0)
+    d = 64
+    viol = 0
+    mism = []
+    for N in (1, 128):
+        for cval in (3, 5, 7):
+            for kexp in range(16):
+                q = np.full((1, 1, N, d), cval * 2.0 ** kexp, np.float32)
+                k = np.ones((1, 1, N, d), np.float32)
+                v = rng.integers(-4, 5, (1, 1, N, d)).astype(np.float32)
+                x = {n: S.f32_to_bf16_bits(a) for n, a in zip(("q", "k", "v"), (q, k, v))}
+                qd, kd, vd = (G.to_dev(x[n]) for n in ("q", "k", "v"))
+                o, _ = gpa.attn_fwd_fma(qd, kd, vd, True, 0.125)
+                o0 = G.to_host(o)[0, 0, 0].astype(np.float32)
+                want = M.historical_fma_one_key(64 * cval * 2 ** kexp, 0.125, v[0, 0, 0])
+                if not np.array_equal(o0, want):
+                    mism.append((N, cval, kexp))
+                viol += int(not np.array_equal(o0, v[0, 0, 0]))
+                osbs, _ = gpa.attn_fwd(qd, kd, vd, True, 0.125)
+                assert np.array_equal(G.bits(osbs)[0, 0, 0], x["v"][0, 0, 0])
+    G.log(f"[historical FMA forward] one-key violations {viol}/96, model mismatches {mism}")
+    assert not mism
+    assert viol > 0
+
+
 # ---------------------------------------------------- tiny workload (cfg 1)
 
 @pytest.mark.parametrize("seed", S.seeds_for(1, 4))

@@ -198,3 +198,26 @@ def test_offset_sweep_floor():
     assert res[1e4][1] > 100 * res[1e4][0]
     assert res[100.0][1] > 5 * res[100.0][0]
     assert res[1e4][1] > 20 * res[100.0][1]
+
+
+def test_historical_fma_argument_is_the_rounding_error():
+    """eq. historical-fma: with x = m, fma(x, a, -fl32(m a)) is exactly the
+    rounding error x a - fl32(x a) (representable in FP32), checked with exact
+    rational arithmetic; the model's one-key output then follows eq.
+    historical-one-key, and equals v exactly when z is 1."""
+    from fractions import Fraction
+    a = np.float32(np.float32(0.125) * np.float32(M.LOG2E))
+    for c in (3, 5, 7):
+        for k in range(16):
+            x = np.float32(64 * c * 2 ** k)
+            prod = Fraction(float(x)) * Fraction(float(a))
+            rounded = Fraction(float(np.float32(x * a)))
+            err = prod - rounded
+            assert Fraction(float(np.float32(float(err)))) == err  # exactly representable
+            v = np.arange(-4, 4, dtype=np.float32)
+            o = M.historical_fma_one_key(x, 0.125, v)
+            z = np.exp2(np.float32(float(err)), dtype=np.float32)
+            if z == np.float32(1.0):
+                assert np.array_equal(o, v)
+            want = M.bf16_round((v * M.bf16_round(z)) / z)
+            assert np.array_equal(o, want)
