@@ -42,17 +42,30 @@ typedef __attribute__((address_space(3))) bf16v4_t lds_bf16v4_t;
 
 // LDS tiles hold 64 rows x D BF16 values, row-major without padding, with the
 // 16-byte chunks of each row permuted: chunk c of row r lives at chunk
-// c ^ swz(r), swz(r) = ((r & 3) << 1) | ((r >> 2) & 1).  Two read patterns hit
-// these tiles: 16-byte reads of one chunk from 8 consecutive rows (rows
-// r..r+7 land on 8 distinct chunk slots) and transpose reads of 32 bytes from
-// 4 consecutive rows (rows 4g..4g+3 land on disjoint chunk pairs); both are
-// free of bank conflicts, and so are the 16-byte staging writes of whole rows.
-__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+// c ^ swz<D>(r).  The gfx950 LDS has 64 banks of 4 bytes (256 bytes per
+// cycle); a 16-byte read is served 16 lanes per cycle and an 8-byte read 32
+// lanes per cycle.  Two read patterns hit these tiles: 16-byte reads of one
+// chunk from 16 consecutive rows, and transpose reads of 32 bytes (two chunks)
+// from 8 consecutive rows.  The swizzle spreads both over 16 distinct 16-byte
+// bank groups:
+//   d = 64  (128-byte rows, two rows per 256-byte bank line): bits 1..3 of the
+//           row pick the chunk within the line for rows of equal parity;
+//   d = 128 (256-byte rows): bits 0..3 of the row pick one of 16 chunks.
+// The staging writes fill whole 256-byte lines and are conflict free anyway.
+// swz<D>(r + 16) == swz<D>(r), so tiles can be addressed 16 rows at a time.
+template <int D>
+__device__ __forceinline__ int swz(int r) {
+    static_assert(D == 64 || D == 128, "head dimension");
+    if constexpr (D == 64)
+        return (((r >> 1) & 3) << 1) | ((r >> 3) & 1);
+    else
+        return ((r & 7) << 1) | ((r >> 3) & 1);
+}
 
 // Element offset of (row r, column col) in a swizzled tile; col % 4 == 0.
 template <int D>
 __device__ __forceinline__ int tile_off(int r, int col) {
-    return r * D + (((col >> 3) ^ swz(r)) << 3) + (col & 7);
+    return r * D + (((col >> 3) ^ swz<D>(r)) << 3) + (col & 7);
 }
 
 // Raw buffer resource over the `bytes` bytes at `base` (stride 0, the gfx9
@@ -133,7 +146,7 @@ struct TileDma {
             const int b = (k * NWAVES + wave) * 1024 + 16 * lane;
             const int r = b / (2 * D);
             const int p = (b - r * 2 * D) / 16;
-            voff[k] = (uint32_t)(r * 2 * D + ((p ^ swz(r)) * 16));
+            voff[k] = (uint32_t)(r * 2 * D + ((p ^ swz<D>(r)) * 16));
             lds[k] = (uint32_t)((k * NWAVES + wave) * 1024);
         }
     }
