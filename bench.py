@@ -141,6 +141,11 @@ def main():
         bwd_ms[m] = timed(lambda: gpa.attn_bwd(q, k, v, o, lse, u, m, w.causal, w.scale,
                                                workspace=ws[m]), args.steps)
     fwd_ms = timed(lambda: gpa.attn_fwd(q, k, v, w.causal, w.scale), args.steps)
+    # The FP32-arithmetic attention (forward + backward in one call, BF16 I/O):
+    # the accuracy-class baseline, timed beside the BF16 path.
+    for _ in range(2):
+        gpa.fp32_attn(q, k, v, u, w.causal, w.scale)
+    fp32_ms = timed(lambda: gpa.fp32_attn(q, k, v, u, w.causal, w.scale), max(5, args.steps // 5))
 
     # Context: the paper's grouped-query capture layout (16 query heads sharing
     # 4 key/value heads, same N, d and input recipe), forward and backward alone.
@@ -195,6 +200,8 @@ def main():
         "bwd_ms": {m: round(t, 5) for m, t in bwd_ms.items()},
         "gproj_bwd_overhead_vs_plain_pct": round(100.0 * (bwd_ms["gproj"] / bwd_ms["plain"] - 1), 2),
         "gproj_q_bwd_overhead_vs_plain_pct": round(100.0 * (bwd_ms["gproj_q"] / bwd_ms["plain"] - 1), 2),
+        "fp32_attn_fwd_bwd_ms": round(fp32_ms, 5),
+        "fp32_attn_vs_gproj_fwd_bwd": round(fp32_ms / (fwd_ms + bwd_ms["gproj"]), 3),
         "wall_s_timed": round(wall, 3),
     }
     if gqa is not None:

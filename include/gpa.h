@@ -181,6 +181,50 @@ gpa_status gpa_attn_bwd_gqa(const uint16_t* Q, const uint16_t* K, const uint16_t
                             void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Packed variable-length sequences (the paper's kernel supports dense and
+ * packed causal layouts, Section 5; its synthetic suite covers packed
+ * segments, unequal lengths, singleton and tile-boundary rows, appendix
+ * "Synthetic Numerical Suite").  nseq sequences are concatenated along the
+ * token axis: sequence s holds tokens [cu_seqlens[s], cu_seqlens[s+1]) and
+ * attention never crosses a sequence boundary (causal: key j visible to
+ * query i of the same sequence iff j <= i).  Each (sequence, query head) is
+ * exactly the problem gpa_attn_fwd_gqa / gpa_attn_bwd_gqa solve for one
+ * head with N = its length, with the same arithmetic and the same kernels.
+ *   Layout     Q, O, dO, dQ [Hq, total, d]; K, V, dK, dV [Hkv, total, d]
+ *              (row t of head h at (h * total + t) * d); LSE and the workspace
+ *              row statistics [Hq, total].  Grouped-query heads as in the
+ *              *_gqa entry points.
+ *   cu_seqlens device int32 array of nseq + 1 offsets, read on the device:
+ *              cu_seqlens[0] = 0, non-decreasing, cu_seqlens[nseq] = total,
+ *              and no sequence longer than max_seqlen (a host value, which
+ *              sizes the grid and the workspace).  Sequences of length 0 are
+ *              allowed.  The kernels clamp every offset to [0, total] and
+ *              every length to max_seqlen, so offsets that break these rules
+ *              cannot make them touch memory outside the tensors; rows no
+ *              sequence covers are then left unwritten and the results are
+ *              unspecified.  cu_seqlens needs 4-byte alignment.
+ *   Shapes     nseq >= 1, 1 <= max_seqlen <= total, Hq*total*d < 2^31,
+ *              nseq*Hq*ceil(max_seqlen/64) < 2^31.
+ * The workspace layout begins like gpa_attn_bwd's with [Hq, total] row
+ * statistics (D, rho, m, lambda at the offsets gpa_bwd_stats_offsets reports
+ * for B = 1, H = Hq, N = total).  Errors as for the *_gqa entry points.
+ */
+gpa_status gpa_attn_fwd_varlen(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                               uint16_t* O, float* LSE, const int32_t* cu_seqlens, int64_t nseq,
+                               int64_t total, int64_t Hq, int64_t Hkv, int64_t max_seqlen,
+                               int64_t d, int causal, float scale, void* stream);
+
+size_t gpa_attn_bwd_varlen_workspace_bytes(int64_t nseq, int64_t total, int64_t Hq, int64_t Hkv,
+                                           int64_t max_seqlen, int64_t d, int mode);
+
+gpa_status gpa_attn_bwd_varlen(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                               const uint16_t* O, const float* LSE, const uint16_t* dO,
+                               uint16_t* dQ, uint16_t* dK, uint16_t* dV,
+                               const int32_t* cu_seqlens, int64_t nseq, int64_t total, int64_t Hq,
+                               int64_t Hkv, int64_t max_seqlen, int64_t d, int causal, float scale,
+                               int mode, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * FP32 attention baseline (the accuracy class of the paper's "FP32 attention",
  * appendix on comparison methods: BF16 inputs and outputs, FP32 SIMT
  * arithmetic, no BF16 or reduced-precision matrix products).  One call runs

@@ -18,6 +18,8 @@ Contents
                         Algorithm 1 backward with the implemented rounding
                         points, used for semantics checks (the -24 witness,
                         mode identities) and to predict error magnitudes.
+  exact_varlen          exact() over packed variable-length sequences (each
+                        sequence its own attention problem).
   rel_l2                the paper's metric: 100 ||G_hat - G64||_2 / ||G64||_2
                         over a full tensor (appendix "Reference and metric").
 """
@@ -127,6 +129,37 @@ def _exact_gqa(lib, Q, K, V, U, causal, scale, nthreads):
     if rc != 0:
         raise RuntimeError(f"oracle_attention_gqa_f64 failed with code {rc}")
     return dict(O=O, LSE=LSE, dQ=dQ, dK=dK, dV=dV)
+
+
+def exact_varlen(q, k, v, do, cu_seqlens, causal: bool, scale: float, nthreads: int = 0):
+    """Exact FP64 attention over packed sequences.
+
+    q, do: [Hq, total, d]; k, v: [Hkv, total, d] (Hkv dividing Hq); sequence
+    s holds tokens cu_seqlens[s] .. cu_seqlens[s+1]-1.  Attention never crosses
+    a sequence boundary, so each sequence is its own attention problem
+    (Section 3.2 with the support L_i restricted to the query's sequence): this
+    slices every sequence out and calls exact() on it.  Returns O, LSE ([Hq,
+    total]), dQ, dK, dV shaped like the inputs; rows outside every sequence
+    are zero.
+    """
+    Q, K, V, U = (as_f64(t) for t in (q, k, v, do))
+    cu = [int(x) for x in np.asarray(cu_seqlens).ravel()]
+    Hq, total, d = Q.shape
+    Hkv = K.shape[0]
+    if K.shape != (Hkv, total, d) or V.shape != K.shape or U.shape != Q.shape or Hq % Hkv:
+        raise ValueError("packed shapes: q, do [Hq, total, d]; k, v [Hkv, total, d]")
+    if cu[0] != 0 or cu[-1] != total or any(b < a for a, b in zip(cu, cu[1:])):
+        raise ValueError("cu_seqlens must start at 0, end at total and be non-decreasing")
+    out = dict(O=np.zeros_like(Q), LSE=np.zeros((Hq, total)), dQ=np.zeros_like(Q),
+               dK=np.zeros_like(K), dV=np.zeros_like(K))
+    for a, b in zip(cu, cu[1:]):
+        if b == a:
+            continue
+        r = exact(Q[None, :, a:b], K[None, :, a:b], V[None, :, a:b], U[None, :, a:b], causal,
+                  scale, nthreads)
+        for n in out:
+            out[n][:, a:b] = r[n][0]
+    return out
 
 
 def rel_l2(approx, target) -> float:

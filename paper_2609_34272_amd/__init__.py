@@ -14,7 +14,10 @@ Python names mirror the C entry points:
   gpa_fp32_attn / fp32_attn               -> O, LSE, dQ, dK, dV (FP32 baseline)
 Grouped-query attention (k, v with fewer heads than q) goes through
 gpa_attn_fwd_gqa / gpa_attn_bwd_gqa / gpa_attn_bwd_gqa_workspace_bytes; the
-same Python functions pick them from the tensor shapes.
+same Python functions pick them from the tensor shapes.  Packed
+variable-length sequences ([H, total, d] tensors with int32 sequence offsets)
+go through gpa_attn_fwd_varlen / gpa_attn_bwd_varlen
+(attn_fwd_varlen / attn_bwd_varlen).
 """
 from __future__ import annotations
 
@@ -26,6 +29,7 @@ import torch  # noqa: F401  (load torch's HIP runtime first; libgpa binds to it)
 
 __all__ = [
     "MODES", "lib", "attn_fwd", "attn_fwd_fma", "attn_bwd", "attn_bwd_workspace_bytes", "bwd_stats_offsets",
+    "attn_fwd_varlen", "attn_bwd_varlen", "attn_bwd_varlen_workspace_bytes",
     "fp32_attn", "fp32_attn_workspace_bytes", "profile_enable", "profile_read", "GpaError",
     "LIB_PATH",
 ]
@@ -74,6 +78,12 @@ def lib():
     L.gpa_attn_bwd_gqa.restype = INT
     L.gpa_attn_bwd_gqa.argtypes = [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, I64, INT, F32,
                                    INT, P, SZ, P]
+    L.gpa_attn_fwd_varlen.restype = INT
+    L.gpa_attn_fwd_varlen.argtypes = [P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, INT, F32, P]
+    L.gpa_attn_bwd_varlen_workspace_bytes.restype = SZ
+    L.gpa_attn_bwd_varlen_workspace_bytes.argtypes = [I64] * 6 + [INT]
+    L.gpa_attn_bwd_varlen.restype = INT
+    L.gpa_attn_bwd_varlen.argtypes = [P] * 10 + [I64] * 6 + [INT, F32, INT, P, SZ, P]
     L.gpa_bwd_stats_offsets.restype = INT
     L.gpa_bwd_stats_offsets.argtypes = [I64, I64, I64, I64, INT] + [ctypes.POINTER(SZ)] * 4
     L.gpa_fp32_attn_workspace_bytes.restype = SZ
@@ -218,6 +228,76 @@ def attn_bwd(q, k, v, o, lse, do, mode: str = "gproj", causal: bool = True, scal
     offs = bwd_stats_offsets(B, H, N, d, mcode)
     n = B * H * N
     stats = {name: workspace[off:off + 4 * n].view(torch.float32).view(B, H, N)
+             for name, off in offs.items()}
+    return dq, dk, dv, stats
+
+
+def _varlen(q, k, cu_seqlens, max_seqlen):
+    """Checks of the packed layout: q [Hq, total, d], k [Hkv, total, d], int32
+    offsets on the GPU.  Returns (nseq, total, Hq, Hkv, d, max_seqlen)."""
+    if q.dim() != 3 or k.dim() != 3 or k.shape[1] != q.shape[1] or k.shape[2] != q.shape[2]:
+        raise ValueError(f"packed q [Hq, total, d] and k [Hkv, total, d] expected, got "
+                         f"{tuple(q.shape)}, {tuple(k.shape)}")
+    Hq, total, d = (int(x) for x in q.shape)
+    Hkv = int(k.shape[0])
+    if Hkv < 1 or Hq % Hkv:
+        raise ValueError(f"query heads {Hq} must be a multiple of key/value heads {Hkv}")
+    if (not cu_seqlens.is_cuda or cu_seqlens.dtype != torch.int32 or cu_seqlens.dim() != 1
+            or cu_seqlens.numel() < 2 or not cu_seqlens.is_contiguous()):
+        raise ValueError("cu_seqlens must be a contiguous 1-D int32 GPU tensor of nseq + 1 offsets")
+    return cu_seqlens.numel() - 1, total, Hq, Hkv, d, int(max_seqlen)
+
+
+def attn_fwd_varlen(q, k, v, cu_seqlens, max_seqlen: int, causal: bool = True, scale=None):
+    """FA3-SBS forward over packed sequences.  q: bf16 [Hq, total, d]; k, v:
+    bf16 [Hkv, total, d]; cu_seqlens: int32 [nseq + 1] offsets on the GPU
+    (sequence s = tokens cu[s] .. cu[s+1]-1); max_seqlen: the longest sequence.
+    Returns O (bf16 [Hq, total, d]) and LSE (float32 [Hq, total])."""
+    nseq, total, Hq, Hkv, d, ms = _varlen(q, k, cu_seqlens, max_seqlen)
+    _need(q, "q", (Hq, total, d), torch.bfloat16)
+    for t, n in ((k, "k"), (v, "v")):
+        _need(t, n, (Hkv, total, d), torch.bfloat16)
+    o = torch.empty_like(q)
+    lse = torch.empty((Hq, total), dtype=torch.float32, device=q.device)
+    _check(lib().gpa_attn_fwd_varlen(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                     lse.data_ptr(), cu_seqlens.data_ptr(), nseq, total, Hq, Hkv,
+                                     ms, d, int(bool(causal)), _scale(d, scale), _stream(q)))
+    return o, lse
+
+
+def attn_bwd_varlen_workspace_bytes(nseq: int, total: int, Hq: int, Hkv: int, max_seqlen: int,
+                                    d: int, mode="gproj") -> int:
+    m = MODES[mode] if isinstance(mode, str) else int(mode)
+    return int(lib().gpa_attn_bwd_varlen_workspace_bytes(nseq, total, Hq, Hkv, max_seqlen, d, m))
+
+
+def attn_bwd_varlen(q, k, v, o, lse, do, cu_seqlens, max_seqlen: int, mode: str = "gproj",
+                    causal: bool = True, scale=None, workspace=None, return_stats: bool = False):
+    """Backward over packed sequences (layouts as attn_fwd_varlen).  Returns
+    dQ, dK, dV; with return_stats=True also FP32 [Hq, total] views D, rho, m,
+    lambda into the workspace."""
+    nseq, total, Hq, Hkv, d, ms = _varlen(q, k, cu_seqlens, max_seqlen)
+    for t, n in ((q, "q"), (o, "o"), (do, "do")):
+        _need(t, n, (Hq, total, d), torch.bfloat16)
+    for t, n in ((k, "k"), (v, "v")):
+        _need(t, n, (Hkv, total, d), torch.bfloat16)
+    _need(lse, "lse", (Hq, total), torch.float32)
+    mcode = MODES[mode] if isinstance(mode, str) else int(mode)
+    nbytes = attn_bwd_varlen_workspace_bytes(nseq, total, Hq, Hkv, ms, d, mcode)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    wsz = workspace.numel() * workspace.element_size()
+    _check(lib().gpa_attn_bwd_varlen(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                     lse.data_ptr(), do.data_ptr(), dq.data_ptr(), dk.data_ptr(),
+                                     dv.data_ptr(), cu_seqlens.data_ptr(), nseq, total, Hq, Hkv, ms,
+                                     d, int(bool(causal)), _scale(d, scale), mcode,
+                                     workspace.data_ptr(), wsz, _stream(q)))
+    if not return_stats:
+        return dq, dk, dv
+    offs = bwd_stats_offsets(1, Hq, total, d, mcode)
+    n = Hq * total
+    stats = {name: workspace[off:off + 4 * n].view(torch.float32).view(Hq, total)
              for name, off in offs.items()}
     return dq, dk, dv, stats
 

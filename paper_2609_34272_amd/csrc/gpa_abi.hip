@@ -112,18 +112,20 @@ struct BwdLayout {
     size_t D, rho, m, lam, ts, z, dkp, dvp, total;
 };
 
-// Four FP32 [B,Hq,N] row statistics; per 64-row query tile a 512-byte block of
-// log2-scaled LSE and D (FP32 [B*Hq, T, 2, 64], T = N rounded up to 64, over
-// 64) that the key-major pass stages with the tile; then (gproj mode only) the
-// BF16 [B,Hq,N,d] tensor z = BF16(lambda q) that the key correction
-// contracts; then, for grouped-query attention (Hq > Hkv) only, the FP32
-// [B,Hq,N,d] per-query-head contributions to dK and dV that the group sum
-// adds.
-BwdLayout bwd_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t d, int mode) {
-    const size_t row = round_up((size_t)B * Hq * N * sizeof(float));
-    const size_t T = (size_t)(N + 63) / 64;
-    const size_t tstats = round_up((size_t)B * Hq * T * 128 * sizeof(float));
-    const size_t part = Hq > Hkv ? round_up((size_t)B * Hq * N * d * sizeof(float)) : 0;
+// Four FP32 row statistics over the query-head rows ([B,Hq,N]; packed
+// sequences [Hq,total]); per problem (query head of one sequence) and 64-row
+// query tile a 512-byte block of log2-scaled LSE and D (FP32 [problems, T, 2,
+// 64], T = the longest sequence rounded up to 64, over 64) that the key-major
+// pass stages with the tile; then (gproj mode only) the BF16 tensor
+// z = BF16(lambda q), shaped like Q, that the key correction contracts; then,
+// for grouped-query attention (Hq > Hkv) only, the FP32 per-query-head
+// contributions to dK and dV (shaped like Q) that the group sum adds.
+BwdLayout bwd_layout_rows(size_t qrows, size_t problems, int64_t Nmax, int64_t d, int mode,
+                          bool grouped) {
+    const size_t row = round_up(qrows * sizeof(float));
+    const size_t T = (size_t)(Nmax + 63) / 64;
+    const size_t tstats = round_up(problems * T * 128 * sizeof(float));
+    const size_t part = grouped ? round_up(qrows * (size_t)d * sizeof(float)) : 0;
     BwdLayout L;
     L.D = 0;
     L.rho = row;
@@ -131,10 +133,57 @@ BwdLayout bwd_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t d, i
     L.lam = 3 * row;
     L.ts = 4 * row;
     L.z = L.ts + tstats;
-    L.dkp = L.z + (mode == 2 ? round_up((size_t)B * Hq * N * d * 2) : 0);
+    L.dkp = L.z + (mode == 2 ? round_up(qrows * (size_t)d * 2) : 0);
     L.dvp = L.dkp + part;
     L.total = L.dvp + part;
     return L;
+}
+
+BwdLayout bwd_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t d, int mode) {
+    return bwd_layout_rows((size_t)B * Hq * N, (size_t)B * Hq, N, d, mode, Hq > Hkv);
+}
+
+// Enqueue the backward passes once the arguments are validated: the
+// query-major pass, the key-major pass and, for grouped-query attention, the
+// group sum of the per-query-head dK, dV contributions.  qrows is the number
+// of query-head rows (the extent of the group-sum partials).
+gpa_status run_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, const uint16_t* O,
+                   const float* LSE, const uint16_t* dO, uint16_t* dQ, uint16_t* dK, uint16_t* dV,
+                   const gpa::Shape& sh, const BwdLayout& L, size_t qrows, int mode,
+                   void* workspace, hipStream_t st) {
+    char* ws = (char*)workspace;
+    float* Drow = (float*)(ws + L.D);
+    float* rho = (float*)(ws + L.rho);
+    float* msum = (float*)(ws + L.m);
+    float* lam = (float*)(ws + L.lam);
+    float* tstats = (float*)(ws + L.ts);
+    uint16_t* zbuf = mode == 2 ? (uint16_t*)(ws + L.z) : nullptr;
+    float* dkp = sh.G > 1 ? (float*)(ws + L.dkp) : nullptr;
+    float* dvp = sh.G > 1 ? (float*)(ws + L.dvp) : nullptr;
+
+    gpa_status s = launched(timed(gpa::kKBwdDq, st,
+                                  [&] {
+                                      return gpa::launch_bwd_dq(Q, K, V, O, dO, LSE, Drow, tstats,
+                                                                dQ, rho, msum, lam, zbuf, mode, sh,
+                                                                st);
+                                  }),
+                            "bwd_dq");
+    if (s != GPA_OK) return s;
+    s = launched(timed(gpa::kKBwdDkdv, st,
+                       [&] {
+                           return gpa::launch_bwd_dkdv(Q, K, V, dO, tstats, zbuf, dK, dV, dkp, dvp,
+                                                       mode, sh, st);
+                       }),
+                 "bwd_dkdv");
+    if (s != GPA_OK || sh.G == 1) return s;
+    // The group sum sees the partials as G consecutive query heads of
+    // qrows / Hq rows each per key/value head.
+    gpa::Shape gs = sh;
+    gs.BH = sh.cu ? sh.Hq : sh.BH;
+    gs.N = (int)(qrows / (size_t)gs.BH);
+    return launched(timed(gpa::kKGroupSum, st,
+                          [&] { return gpa::launch_bwd_group_sum(dkp, dvp, dK, dV, gs, st); }),
+                    "group_sum");
 }
 
 gpa_status check_heads(int64_t Hq, int64_t Hkv) {
@@ -144,6 +193,41 @@ gpa_status check_heads(int64_t Hq, int64_t Hkv) {
     return GPA_OK;
 }
 
+// Packed variable-length sequences.
+gpa_status check_varlen(const int32_t* cu, int64_t nseq, int64_t total, int64_t Hq, int64_t Hkv,
+                        int64_t max_seqlen, int64_t d, float scale) {
+    if (nseq < 1 || total < 1 || max_seqlen < 1 || max_seqlen > total)
+        return fail(GPA_EINVAL,
+                    "need nseq >= 1, total >= 1 and 1 <= max_seqlen <= total (got %lld, %lld, %lld)",
+                    (long long)nseq, (long long)total, (long long)max_seqlen);
+    gpa_status s = check_shape(1, Hq, total, d, scale);
+    if (s != GPA_OK) return s;
+    if ((s = check_heads(Hq, Hkv)) != GPA_OK) return s;
+    if (!cu) return fail(GPA_EINVAL, "cu_seqlens is NULL");
+    if ((uintptr_t)cu % 4) return fail(GPA_EINVAL, "cu_seqlens is not 4-byte aligned");
+    const double grid = (double)nseq * (double)Hq * (double)((max_seqlen + 63) / 64);
+    if (grid >= 2147483648.0 || (double)nseq * Hq >= 2147483648.0)
+        return fail(GPA_EINVAL, "nseq * Hq * ceil(max_seqlen / 64) = %.0f exceeds 2^31 - 1", grid);
+    return GPA_OK;
+}
+
+// The sequence offsets are an input: no output may overlap them.
+gpa_status check_cu_overlap(const int32_t* cu, int64_t nseq, const std::vector<Buf>& outs) {
+    const Buf c{cu, 4 * (size_t)(nseq + 1), "cu_seqlens"};
+    for (const Buf& b : outs)
+        if (overlap(b, c)) return fail(GPA_EINVAL, "%s overlaps cu_seqlens", b.name);
+    return GPA_OK;
+}
+
+gpa::Shape varlen_shape(const int32_t* cu, int64_t nseq, int64_t total, int64_t Hq, int64_t Hkv,
+                        int64_t max_seqlen, int64_t d, int causal, float scale) {
+    gpa::Shape sh{(int)(nseq * Hq), (int)max_seqlen, (int)d, causal ? 1 : 0, scale,
+                  (int)(Hq / Hkv)};
+    sh.cu = cu;
+    sh.Hq = (int)Hq;
+    sh.total = (int)total;
+    return sh;
+}
 }  // namespace
 
 extern "C" {
@@ -248,35 +332,8 @@ gpa_status gpa_attn_bwd_gqa(const uint16_t* Q, const uint16_t* K, const uint16_t
     if (s != GPA_OK) return s;
 
     const gpa::Shape sh{(int)(B * Hq), (int)N, (int)d, causal ? 1 : 0, scale, (int)(Hq / Hkv)};
-    hipStream_t st = (hipStream_t)stream;
-    const BwdLayout L = bwd_layout(B, Hq, Hkv, N, d, mode);
-    char* ws = (char*)workspace;
-    float* Drow = (float*)(ws + L.D);
-    float* rho = (float*)(ws + L.rho);
-    float* msum = (float*)(ws + L.m);
-    float* lam = (float*)(ws + L.lam);
-    float* tstats = (float*)(ws + L.ts);
-    uint16_t* zbuf = mode == 2 ? (uint16_t*)(ws + L.z) : nullptr;
-    float* dkp = sh.G > 1 ? (float*)(ws + L.dkp) : nullptr;
-    float* dvp = sh.G > 1 ? (float*)(ws + L.dvp) : nullptr;
-
-    s = launched(timed(gpa::kKBwdDq, st,
-                       [&] {
-                           return gpa::launch_bwd_dq(Q, K, V, O, dO, LSE, Drow, tstats, dQ, rho, msum,
-                                                     lam, zbuf, mode, sh, st);
-                       }),
-                 "bwd_dq");
-    if (s != GPA_OK) return s;
-    s = launched(timed(gpa::kKBwdDkdv, st,
-                       [&] {
-                           return gpa::launch_bwd_dkdv(Q, K, V, dO, tstats, zbuf, dK, dV, dkp, dvp,
-                                                       mode, sh, st);
-                       }),
-                 "bwd_dkdv");
-    if (s != GPA_OK || sh.G == 1) return s;
-    return launched(timed(gpa::kKGroupSum, st,
-                          [&] { return gpa::launch_bwd_group_sum(dkp, dvp, dK, dV, sh, st); }),
-                    "group_sum");
+    return run_bwd(Q, K, V, O, LSE, dO, dQ, dK, dV, sh, bwd_layout(B, Hq, Hkv, N, d, mode),
+                   (size_t)B * Hq * N, mode, workspace, (hipStream_t)stream);
 }
 
 gpa_status gpa_attn_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
@@ -286,6 +343,68 @@ gpa_status gpa_attn_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                         size_t workspace_bytes, void* stream) {
     return gpa_attn_bwd_gqa(Q, K, V, O, LSE, dO, dQ, dK, dV, B, H, H, N, d, causal, scale, mode,
                             workspace, workspace_bytes, stream);
+}
+
+
+gpa_status gpa_attn_fwd_varlen(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                               uint16_t* O, float* LSE, const int32_t* cu_seqlens, int64_t nseq,
+                               int64_t total, int64_t Hq, int64_t Hkv, int64_t max_seqlen,
+                               int64_t d, int causal, float scale, void* stream) {
+    gpa_status s = check_varlen(cu_seqlens, nseq, total, Hq, Hkv, max_seqlen, d, scale);
+    if (s != GPA_OK) return s;
+    const size_t tq = (size_t)Hq * total * d * 2, tkv = (size_t)Hkv * total * d * 2;
+    const size_t lb = (size_t)Hq * total * 4;
+    s = check_ptrs({{Q, tq, "Q"}, {K, tkv, "K"}, {V, tkv, "V"}}, {{O, tq, "O"}, {LSE, lb, "LSE"}});
+    if (s != GPA_OK) return s;
+    if ((s = check_cu_overlap(cu_seqlens, nseq, {{O, tq, "O"}, {LSE, lb, "LSE"}})) != GPA_OK)
+        return s;
+    const gpa::Shape sh = varlen_shape(cu_seqlens, nseq, total, Hq, Hkv, max_seqlen, d, causal, scale);
+    hipStream_t st = (hipStream_t)stream;
+    return launched(timed(gpa::kKFwd, st, [&] { return gpa::launch_fwd(Q, K, V, O, LSE, sh, st); }),
+                    "fwd_sbs");
+}
+
+size_t gpa_attn_bwd_varlen_workspace_bytes(int64_t nseq, int64_t total, int64_t Hq, int64_t Hkv,
+                                           int64_t max_seqlen, int64_t d, int mode) {
+    if (mode < 0 || mode > 2) return 0;
+    if (nseq < 1 || total < 1 || max_seqlen < 1 || max_seqlen > total) return 0;
+    if (Hq < 1 || Hkv < 1 || Hq % Hkv || (d != 64 && d != 128)) return 0;
+    if ((double)Hq * total * d >= 2147483648.0) return 0;
+    if ((double)nseq * Hq * (double)((max_seqlen + 63) / 64) >= 2147483648.0) return 0;
+    return bwd_layout_rows((size_t)Hq * total, (size_t)nseq * Hq, max_seqlen, d, mode, Hq > Hkv)
+        .total;
+}
+
+gpa_status gpa_attn_bwd_varlen(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                               const uint16_t* O, const float* LSE, const uint16_t* dO,
+                               uint16_t* dQ, uint16_t* dK, uint16_t* dV,
+                               const int32_t* cu_seqlens, int64_t nseq, int64_t total, int64_t Hq,
+                               int64_t Hkv, int64_t max_seqlen, int64_t d, int causal, float scale,
+                               int mode, void* workspace, size_t workspace_bytes, void* stream) {
+    gpa_status s = check_varlen(cu_seqlens, nseq, total, Hq, Hkv, max_seqlen, d, scale);
+    if (s != GPA_OK) return s;
+    if (mode < 0 || mode > 2) return fail(GPA_EINVAL, "mode %d is not 0, 1 or 2", mode);
+    const size_t need =
+        gpa_attn_bwd_varlen_workspace_bytes(nseq, total, Hq, Hkv, max_seqlen, d, mode);
+    if (!workspace || workspace_bytes < need)
+        return fail(GPA_EWORKSPACE, "workspace %p of %zu bytes; %zu needed", workspace,
+                    workspace_bytes, need);
+    if ((uintptr_t)workspace % kAlign)
+        return fail(GPA_EWORKSPACE, "workspace is not %zu-byte aligned", kAlign);
+    const size_t tq = (size_t)Hq * total * d * 2, tkv = (size_t)Hkv * total * d * 2;
+    const size_t lb = (size_t)Hq * total * 4;
+    const std::vector<Buf> outs = {
+        {dQ, tq, "dQ"}, {dK, tkv, "dK"}, {dV, tkv, "dV"}, {workspace, need, "workspace"}};
+    s = check_ptrs({{Q, tq, "Q"}, {K, tkv, "K"}, {V, tkv, "V"}, {O, tq, "O"}, {LSE, lb, "LSE"},
+                    {dO, tq, "dO"}},
+                   outs);
+    if (s != GPA_OK) return s;
+    if ((s = check_cu_overlap(cu_seqlens, nseq, outs)) != GPA_OK) return s;
+    const gpa::Shape sh = varlen_shape(cu_seqlens, nseq, total, Hq, Hkv, max_seqlen, d, causal, scale);
+    const BwdLayout L =
+        bwd_layout_rows((size_t)Hq * total, (size_t)nseq * Hq, max_seqlen, d, mode, Hq > Hkv);
+    return run_bwd(Q, K, V, O, LSE, dO, dQ, dK, dV, sh, L, (size_t)Hq * total, mode, workspace,
+                   (hipStream_t)stream);
 }
 
 size_t gpa_fp32_attn_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d) {

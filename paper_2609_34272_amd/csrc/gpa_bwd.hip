@@ -101,7 +101,8 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     const uint16_t* __restrict__ dO, const float* __restrict__ LSE, float* __restrict__ D_out,
     float* __restrict__ TS, uint16_t* __restrict__ dQ,
     float* __restrict__ rho_out, float* __restrict__ m_out, float* __restrict__ lam_out,
-    uint16_t* __restrict__ Zout, int BH, int N, int causal, float scale, int G) {
+    uint16_t* __restrict__ Zout, int BH, int Nmax, int causal, float scale, int G,
+    const int* __restrict__ cu, int Hq, int total) {
     constexpr int MB = D / 16;  // 16-column blocks of d
     constexpr int KC = D / 32;  // 32-wide k chunks of d
     constexpr int PER_NB = 2 * MB * 4 + 2;  // partial A, B (interleaved) and rho, m
@@ -113,12 +114,16 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     __shared__ __attribute__((aligned(16))) uint16_t S1[2 * TILE_E];
     __shared__ __attribute__((aligned(16))) uint16_t S2[2 * TILE_E];
 
-    const int T = (N + kTile - 1) / kTile;
+    const int T = (Nmax + kTile - 1) / kTile;  // tiles of the longest problem
     int bh, tile;
     map_block(blockIdx.x, BH, T, causal != 0, &bh, &tile);
-    const size_t hoff = (size_t)bh * N * D;        // query head
-    const size_t kvoff = (size_t)(bh / G) * N * D;  // its key/value head
-    const size_t soff = (size_t)bh * N;
+    const SeqRows sr = seq_rows(cu, bh, Nmax, G, Hq, total);
+    const int N = sr.n;
+    if (tile * kTile >= N) return;  // a shorter sequence has no such tile
+    const int Tn = (N + kTile - 1) / kTile;
+    const size_t hoff = sr.q0 * D;    // query head
+    const size_t kvoff = sr.kv0 * D;  // its key/value head
+    const size_t soff = sr.q0;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -172,7 +177,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
         accM[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
 
-    const int nkv = causal ? min(T, tile + 1) : T;
+    const int nkv = causal ? min(Tn, tile + 1) : Tn;
     // Only the last key tile can need masks: the diagonal tile (causal) or the
     // key tail (N not a multiple of the tile).  Query rows beyond N need none
     // (their P is 0 and they are not stored).
@@ -386,8 +391,8 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
     const float* __restrict__ TS, const uint16_t* __restrict__ Z, uint16_t* __restrict__ dK,
-    uint16_t* __restrict__ dV, float* __restrict__ dKp, float* __restrict__ dVp, int BH, int N,
-    int causal, float scale, int G) {
+    uint16_t* __restrict__ dV, float* __restrict__ dKp, float* __restrict__ dVp, int BH, int Nmax,
+    int causal, float scale, int G, const int* __restrict__ cu, int Hq, int total) {
     constexpr int MB = D / 16;
     constexpr int KC = D / 32;
     constexpr int NT = GPROJ ? 3 : 2;  // staged tensors: Q, dO (and Z = BF16(lambda Q))
@@ -405,12 +410,16 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     __shared__ __attribute__((aligned(16))) uint16_t B1[SLOT_E];
     __shared__ __attribute__((aligned(16))) uint16_t B2[SLOT_E];
 
-    const int T = (N + kTile - 1) / kTile;
+    const int Tmax = (Nmax + kTile - 1) / kTile;  // tiles of the longest problem
     int bh, tile;
-    map_block(blockIdx.x, BH, T, false, &bh, &tile);
-    const size_t hoff = (size_t)bh * N * D;        // query head: Q, dO, z, partials
-    const size_t kvoff = (size_t)(bh / G) * N * D;  // its key/value head: K, V, dK, dV
-    const float* tsh = TS + (size_t)bh * T * kStatFloats;
+    map_block(blockIdx.x, BH, Tmax, false, &bh, &tile);
+    const SeqRows sr = seq_rows(cu, bh, Nmax, G, Hq, total);
+    const int N = sr.n;
+    if (tile * kTile >= N) return;  // a shorter sequence has no such tile
+    const int T = (N + kTile - 1) / kTile;
+    const size_t hoff = sr.q0 * D;    // query head: Q, dO, z, partials
+    const size_t kvoff = sr.kv0 * D;  // its key/value head: K, V, dK, dV
+    const float* tsh = TS + (size_t)bh * Tmax * kStatFloats;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -694,7 +703,7 @@ hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V
 #define GPA_DQ(DD, GP, WZ)                                                                   \
     bwd_dq_kernel<DD, GP, WZ><<<grid, block, 0, st>>>(Q, K, V, O, dO, LSE, Drow, TS, dQ, rho, \
                                                       msum, lambda, Z, s.BH, s.N, s.causal,  \
-                                                      s.scale, s.G)
+                                                      s.scale, s.G, s.cu, s.Hq, s.total)
     if (s.d == 64) {
         if (mode == 2) GPA_DQ(64, true, true);
         else if (mode == 1) GPA_DQ(64, true, false);
@@ -717,7 +726,8 @@ hipError_t launch_bwd_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t*
     const bool gp = mode == 2;
 #define GPA_DKDV(DD, GP)                                                             \
     bwd_dkdv_kernel<DD, GP><<<grid, block, 0, st>>>(Q, K, V, dO, TS, Z, dK, dV, dKp, dVp, \
-                                                    s.BH, s.N, s.causal, s.scale, s.G)
+                                                    s.BH, s.N, s.causal, s.scale, s.G, s.cu, \
+                                                    s.Hq, s.total)
     if (s.d == 64) {
         if (gp) GPA_DKDV(64, true); else GPA_DKDV(64, false);
     } else {

@@ -302,6 +302,26 @@ __device__ __forceinline__ void map_block(int bid, int BH, int T, bool heavy_hig
     *tile = heavy_high ? (T - 1 - rank) : rank;
 }
 
+// Rows of one attention problem (a query head of one sequence) and the number
+// of its tokens.  Dense batches ([B, H, N, d], cu == nullptr): query head
+// bh = b * Hq + h starts at row bh * N of Q and reads key/value head bh / G.
+// Packed sequences ([H, total, d]): bh = s * Hq + h is head h over tokens
+// [cu[s], cu[s + 1]); the offsets are clamped to [0, total] and the length to
+// Nmax, so malformed offsets cannot address rows outside the tensors.
+struct SeqRows {
+    size_t q0;   // first row of the query-head tensors (Q, O, dO, dQ; LSE and row statistics)
+    size_t kv0;  // first row of the key/value-head tensors (K, V, dK, dV)
+    int n;       // tokens of this problem
+};
+__device__ __forceinline__ SeqRows seq_rows(const int* cu, int bh, int Nmax, int G, int Hq,
+                                            int total) {
+    if (cu == nullptr) return {(size_t)bh * Nmax, (size_t)(bh / G) * Nmax, Nmax};
+    const int s = bh / Hq, h = bh - s * Hq;
+    const int a = min(max(cu[s], 0), total);
+    const int b = min(max(cu[s + 1], a), total);
+    return {(size_t)h * total + a, (size_t)(h / G) * total + a, min(b - a, Nmax)};
+}
+
 // Target waves per SIMD of each MFMA kernel (build-time tuning constants).
 #ifndef GPA_FWD_OCC
 #define GPA_FWD_OCC 2

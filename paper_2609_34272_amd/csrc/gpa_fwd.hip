@@ -44,7 +44,8 @@ template <int D, bool FMA>
 __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, uint16_t* __restrict__ O, float* __restrict__ LSE,
-    int BH, int N, int causal, float scale, int G) {
+    int BH, int Nmax, int causal, float scale, int G, const int* __restrict__ cu, int Hq,
+    int total) {
     constexpr int MB = D / 16;
     constexpr int KC = D / 32;
     constexpr int PER_NB = MB * 4 + 2;  // acc, m, l of one query block
@@ -53,11 +54,14 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
     __shared__ __attribute__((aligned(16))) uint16_t KV0[2][kTile * D];
     __shared__ __attribute__((aligned(16))) uint16_t KV1[2][kTile * D];
 
-    const int T = (N + kTile - 1) / kTile;
+    const int T = (Nmax + kTile - 1) / kTile;  // tiles of the longest problem
     int bh, tile;
     map_block(blockIdx.x, BH, T, causal != 0, &bh, &tile);
-    const size_t hoff = (size_t)bh * N * D;        // query head: Q, O
-    const size_t kvoff = (size_t)(bh / G) * N * D;  // its key/value head
+    const SeqRows sr = seq_rows(cu, bh, Nmax, G, Hq, total);
+    const int N = sr.n;
+    if (tile * kTile >= N) return;  // a shorter sequence has no such tile
+    const size_t hoff = sr.q0 * D;    // query head: Q, O
+    const size_t kvoff = sr.kv0 * D;  // its key/value head
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -248,7 +252,7 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
             if (g == 0) {
 #pragma clang fp contract(off)
                 const float lse = scale * mt + logf(ltot);
-                LSE[(size_t)bh * N + qrow] = lse;
+                LSE[sr.q0 + qrow] = lse;
             }
         }
     }
@@ -265,17 +269,21 @@ template <int D, bool FMA>
 __global__ __launch_bounds__(kThreads, GPA_FWD16_OCC) void fwd_sbs_q16_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, uint16_t* __restrict__ O, float* __restrict__ LSE,
-    int BH, int N, int causal, float scale, int G) {
+    int BH, int Nmax, int causal, float scale, int G, const int* __restrict__ cu, int Hq,
+    int total) {
     constexpr int MB = D / 16;
     constexpr int KC = D / 32;
     __shared__ __attribute__((aligned(16))) uint16_t KV0[2][kTile * D];
     __shared__ __attribute__((aligned(16))) uint16_t KV1[2][kTile * D];
 
-    const int T = (N + kTile - 1) / kTile;
+    const int T = (Nmax + kTile - 1) / kTile;  // tiles of the longest problem
     int bh, tile;
     map_block(blockIdx.x, BH, T, causal != 0, &bh, &tile);
-    const size_t hoff = (size_t)bh * N * D;
-    const size_t kvoff = (size_t)(bh / G) * N * D;
+    const SeqRows sr = seq_rows(cu, bh, Nmax, G, Hq, total);
+    const int N = sr.n;
+    if (tile * kTile >= N) return;  // a shorter sequence has no such tile
+    const size_t hoff = sr.q0 * D;
+    const size_t kvoff = sr.kv0 * D;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -395,7 +403,7 @@ __global__ __launch_bounds__(kThreads, GPA_FWD16_OCC) void fwd_sbs_q16_kernel(
         if (g == 0) {
 #pragma clang fp contract(off)
             const float lse = scale * mrun + logf(ltot);
-            LSE[(size_t)bh * N + qrow] = lse;
+            LSE[sr.q0 + qrow] = lse;
         }
     }
 }
@@ -409,7 +417,8 @@ hipError_t launch_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, u
     // d = 64: one 16-query block per wave (measured faster); d = 128: two
     // blocks per wave, whose halved LDS reads matter more there.
 #define GPA_FWD(KERNEL, DD, FM)                                                               \
-    KERNEL<DD, FM><<<grid, block, 0, st>>>(Q, K, V, O, LSE, s.BH, s.N, s.causal, s.scale, s.G)
+    KERNEL<DD, FM><<<grid, block, 0, st>>>(Q, K, V, O, LSE, s.BH, s.N, s.causal, s.scale, s.G, \
+                                           s.cu, s.Hq, s.total)
     if (s.d == 64) {
         if (fma_forward) GPA_FWD(fwd_sbs_q16_kernel, 64, true);
         else GPA_FWD(fwd_sbs_q16_kernel, 64, false);

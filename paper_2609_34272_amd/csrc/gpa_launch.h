@@ -8,13 +8,19 @@
 namespace gpa {
 
 struct Shape {
-    int BH;        // batch * query heads
-    int N;         // sequence length
+    int BH;        // batch * query heads (packed sequences: sequences * query heads)
+    int N;         // sequence length (packed sequences: the longest one)
     int d;         // head dimension (64 or 128)
     int causal;    // 1: key j visible to query i iff j <= i
     float scale;   // attention scale alpha
     int G;         // query heads per key/value head (1: multi-head attention);
                    // query head bh reads key/value head bh / G
+    // Packed variable-length sequences (nullptr: dense [B, H, N, d] batches).
+    // Tensors are [H, total, d]; sequence s holds tokens [cu[s], cu[s + 1]) and
+    // problem bh = s * Hq + h is head h of sequence s.
+    const int* cu = nullptr;  // device, nseq + 1 offsets
+    int Hq = 1;               // query heads
+    int total = 0;            // tokens in the packed tensors
 };
 
 // Kernel ids for timing (gpa_profile_*).

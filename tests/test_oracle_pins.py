@@ -312,3 +312,75 @@ def test_gqa_conservation_and_per_head_identity():
                     one = _exact_head(q[b, h], k[b, j], v[b, j], u[b, h], causal, 0.6)
                     for n in ("O", "LSE", "dQ"):
                         assert np.array_equal(ex[n][b, h], one[n])
+
+
+# ------------------------------------------------------- packed sequences
+
+def _decimal_packed_loss(q, k, v, u, seg, causal, alpha, G, dirs=None, h=None, prec=40):
+    """L = sum O*u over packed heads by direct softmax in decimal arithmetic,
+    with the visibility written as a mask over the whole packed axis: key j is
+    visible to query i iff seg[i] == seg[j] (and j <= i when causal).  Query
+    head hq reads key/value head hq // G.  Returns (O, LSE, L)."""
+    ctx = decimal.Context(prec=prec)
+    D = lambda x: ctx.create_decimal(repr(float(x)))  # noqa: E731
+    Hq, T, d = q.shape
+
+    def lift(x, dx):
+        out = [[[D(x[a, i, c]) for c in range(d)] for i in range(T)] for a in range(x.shape[0])]
+        if dx is not None:
+            out = [[[out[a][i][c] + h * D(dx[a, i, c]) for c in range(d)] for i in range(T)]
+                   for a in range(x.shape[0])]
+        return out
+
+    dq_, dk_, dv_ = dirs if dirs is not None else (None, None, None)
+    Qd, Kd, Vd = lift(q, dq_), lift(k, dk_), lift(v, dv_)
+    a = D(alpha)
+    O = np.zeros(q.shape)
+    LSE = np.zeros((Hq, T))
+    Ltot = D(0)
+    for hq in range(Hq):
+        hk = hq // G
+        for i in range(T):
+            vis = [j for j in range(T) if seg[j] == seg[i] and (not causal or j <= i)]
+            s = [a * sum((Qd[hq][i][c] * Kd[hk][j][c] for c in range(d)), D(0)) for j in vis]
+            e = [ctx.exp(x) for x in s]
+            Z = sum(e, D(0))
+            LSE[hq, i] = float(ctx.ln(Z))
+            for c in range(d):
+                oc = sum((e[n] * Vd[hk][j][c] for n, j in enumerate(vis)), D(0)) / Z
+                O[hq, i, c] = float(oc)
+                Ltot += oc * D(u[hq, i, c])
+    return O, LSE, Ltot
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_packed_oracle_matches_masked_brute_force(causal):
+    """exact_varlen (per-sequence slices) against a brute force over the whole
+    packed axis with a sequence mask: forward values and the directional
+    derivative of L = sum O*dO, with grouped-query heads, empty and singleton
+    sequences."""
+    rng = np.random.default_rng(21)
+    lens = [3, 0, 1, 4, 2]
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    T, d, Hq, Hkv, alpha = int(cu[-1]), 3, 2, 1, 0.8
+    seg = np.repeat(np.arange(len(lens)), lens)
+    q = rng.standard_normal((Hq, T, d)) * 1.5
+    k = rng.standard_normal((Hkv, T, d)) + 2.0 * rng.standard_normal(d)
+    v = rng.standard_normal((Hkv, T, d))
+    u = rng.standard_normal((Hq, T, d))
+    ex = oracle.exact_varlen(q, k, v, u, cu, causal, alpha)
+    O, LSE, _ = _decimal_packed_loss(q, k, v, u, seg, causal, alpha, Hq // Hkv)
+    assert np.allclose(ex["O"], O, rtol=0, atol=1e-13)
+    assert np.allclose(ex["LSE"], LSE, rtol=0, atol=1e-13)
+    dirs = (rng.standard_normal(q.shape), rng.standard_normal(k.shape), rng.standard_normal(v.shape))
+    h = decimal.Decimal("1e-15")
+    _, _, Lp = _decimal_packed_loss(q, k, v, u, seg, causal, alpha, Hq // Hkv, dirs=dirs, h=h)
+    _, _, Lm = _decimal_packed_loss(q, k, v, u, seg, causal, alpha, Hq // Hkv, dirs=dirs, h=-h)
+    fd = float((Lp - Lm) / (2 * h))
+    an = float(sum(np.sum(g * dd) for g, dd in zip((ex["dQ"], ex["dK"], ex["dV"]), dirs)))
+    assert abs(fd - an) <= 1e-10 * max(1.0, abs(an))
+    # a singleton sequence sees only itself: its output is its value row, its
+    # query gradient is zero
+    one = int(cu[2])
+    assert np.array_equal(ex["O"][:, one], np.repeat(v[:, one], Hq // Hkv, axis=0))
+    assert np.all(ex["dQ"][:, one] == 0.0)
