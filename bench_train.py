@@ -1,0 +1,172 @@
+#!/usr/bin/env python3
+"""Training-step benchmark: a synthetic decoder model with this library's
+attention, timed per backward mode.
+
+Mirrors the protocol of the paper's cost comparison (appendix on accuracy and
+cost, "Timing"): one causal sequence of 4096 tokens, batch one, 16 query heads
+sharing 4 key/value heads, d = 64, FP32 master weights with BF16 compute
+(autocast), AdamW, gradient clipping at one and activation checkpointing per
+layer, so a step runs two attention forwards (one of them the recomputation)
+and one attention backward per layer: 48 forwards and 24 backwards for 24
+layers.  The model is this script's own stand-in with about 0.43 B parameters
+(d_model 1024, SwiGLU width 4096, vocabulary 32000, RMSNorm, no positional
+encoding), randomly initialised and fed random tokens: only the step time
+means anything.  Everything except attention runs on PyTorch's own kernels.
+
+Prints one JSON line with the mean step time per mode (plain, gproj_q,
+gproj; modes interleaved over rounds), the GProj overhead over plain and the
+attention share measured with the library's kernel timers.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--steps", type=int, default=10, help="timed steps per mode and round")
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--rounds", type=int, default=3)
+    p.add_argument("--layers", type=int, default=24)
+    p.add_argument("--seq", type=int, default=4096)
+    return p.parse_args()
+
+
+def build_model(torch, gpa, layers, vocab=32000, dm=1024, hq=16, hkv=4, dh=64, ff=4096):
+    nn = torch.nn
+    from torch.utils.checkpoint import checkpoint
+
+    class RMSNorm(nn.Module):
+        def __init__(self, n):
+            super().__init__()
+            self.w = nn.Parameter(torch.ones(n))
+
+        def forward(self, x):
+            xf = x.float()
+            return (xf * torch.rsqrt(xf.pow(2).mean(-1, keepdim=True) + 1e-6) * self.w).to(x.dtype)
+
+    class Block(nn.Module):
+        def __init__(self):
+            super().__init__()
+            self.n1, self.n2 = RMSNorm(dm), RMSNorm(dm)
+            self.qkv = nn.Linear(dm, (hq + 2 * hkv) * dh, bias=False)
+            self.o = nn.Linear(hq * dh, dm, bias=False)
+            self.w13 = nn.Linear(dm, 2 * ff, bias=False)
+            self.w2 = nn.Linear(ff, dm, bias=False)
+            self.mode = "gproj"
+
+        def attn(self, h):
+            N = h.shape[0]
+            qkv = self.qkv(h).view(N, hq + 2 * hkv, dh).transpose(0, 1)
+            q = qkv[:hq].unsqueeze(0).contiguous()
+            k = qkv[hq:hq + hkv].unsqueeze(0).contiguous()
+            v = qkv[hq + hkv:].unsqueeze(0).contiguous()
+            o = gpa.attention(q, k, v, True, 1.0 / dh ** 0.5, self.mode)
+            return self.o(o[0].transpose(0, 1).reshape(N, hq * dh))
+
+        def body(self, x):
+            x = x + self.attn(self.n1(x))
+            a, b = self.w13(self.n2(x)).chunk(2, dim=-1)
+            return x + self.w2(torch.nn.functional.silu(a) * b)
+
+        def forward(self, x):
+            return checkpoint(self.body, x, use_reentrant=False)
+
+    class Model(nn.Module):
+        def __init__(self):
+            super().__init__()
+            self.emb = nn.Embedding(vocab, dm)
+            self.blocks = nn.ModuleList(Block() for _ in range(layers))
+            self.norm = RMSNorm(dm)
+            self.head = nn.Linear(dm, vocab, bias=False)
+
+        def forward(self, tok):
+            x = self.emb(tok)
+            for b in self.blocks:
+                x = b(x)
+            return self.head(self.norm(x))
+
+    return Model()
+
+
+def main():
+    args = parse()
+    import torch
+    import paper_2609_34272_amd as gpa
+
+    if not torch.cuda.is_available():
+        print("bench_train.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    gpa.lib()
+    dev = torch.device("cuda:0")
+    torch.manual_seed(0)
+    model = build_model(torch, gpa, args.layers).to(dev)
+    nparams = sum(p.numel() for p in model.parameters())
+    opt = torch.optim.AdamW(model.parameters(), lr=1e-4, weight_decay=0.1, fused=True)
+    g = torch.Generator(device=dev).manual_seed(1)
+    tok = torch.randint(0, 32000, (args.seq + 1,), device=dev, generator=g)
+
+    def set_mode(m):
+        for b in model.blocks:
+            b.mode = m
+
+    def step():
+        with torch.autocast("cuda", dtype=torch.bfloat16):
+            logits = model(tok[:-1])
+        loss = torch.nn.functional.cross_entropy(logits.float(), tok[1:])
+        loss.backward()
+        torch.nn.utils.clip_grad_norm_(model.parameters(), 1.0)
+        opt.step()
+        opt.zero_grad(set_to_none=True)
+        return loss
+
+    modes = ["plain", "gproj_q", "gproj"]
+    for m in modes:
+        set_mode(m)
+        for _ in range(args.warmup):
+            step()
+    torch.cuda.synchronize()
+    times = {m: [] for m in modes}
+    for _ in range(args.rounds):
+        for m in modes:
+            set_mode(m)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(args.steps):
+                step()
+            e1.record()
+            torch.cuda.synchronize()
+            times[m].append(e0.elapsed_time(e1) / args.steps)
+    ms = {m: sorted(t)[len(t) // 2] for m, t in times.items()}
+    # attention kernel time inside one gproj step
+    set_mode("gproj")
+    gpa.profile_enable(True)
+    step()
+    torch.cuda.synchronize()
+    prof = gpa.profile_read()
+    gpa.profile_enable(False)
+    attn_ms = sum(t for t, c in prof.values())
+    calls = {k: c for k, (t, c) in prof.items() if c}
+    out = {
+        "metric": "training step ms, synthetic 0.43B decoder (B=1, N=4096, 16/4 heads, d=64)",
+        "unit": "ms", "higher_is_better": False, "data": "synthetic",
+        "params": nparams, "layers": args.layers, "seq": args.seq,
+        "ms_per_step": {m: round(v, 3) for m, v in ms.items()},
+        "ms_per_step_rounds": {m: [round(x, 3) for x in v] for m, v in times.items()},
+        "gproj_step_overhead_vs_plain_pct": round(100 * (ms["gproj"] / ms["plain"] - 1), 2),
+        "gproj_q_step_overhead_vs_plain_pct": round(100 * (ms["gproj_q"] / ms["plain"] - 1), 2),
+        "attention_ms_per_gproj_step": round(attn_ms, 3),
+        "attention_launches_per_step": calls,
+        "peak_allocated_gib": round(torch.cuda.max_memory_allocated() / 2 ** 30, 3),
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -31,7 +31,7 @@ __all__ = [
     "MODES", "lib", "attn_fwd", "attn_fwd_fma", "attn_bwd", "attn_bwd_workspace_bytes", "bwd_stats_offsets",
     "attn_fwd_varlen", "attn_bwd_varlen", "attn_bwd_varlen_workspace_bytes",
     "fp32_attn", "fp32_attn_workspace_bytes", "profile_enable", "profile_read", "GpaError",
-    "LIB_PATH",
+    "LIB_PATH", "attention", "attention_varlen",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -336,6 +336,8 @@ def profile_read():
     k = lib().gpa_profile_read(ms, cnt, n)
     return {lib().gpa_kernel_name(i).decode(): (ms[i], cnt[i]) for i in range(k)}
 
+
+from .autograd import attention, attention_varlen  # noqa: E402
 
 # Raw C entry points under their C names (argument marshalling is the caller's).
 def __getattr__(name):
