@@ -213,6 +213,13 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
         const uint16_t* Kc = cur;
         const uint16_t* Vc = cur + TILE_E;
         fill_piece(nxt2, kt + 2, 0);
+        // In the gproj modes the transposed K operands of the A/B products are
+        // read now, so their LDS latency hides behind the S/dP products and the
+        // exponentials (measured faster there, slower in plain mode).
+        constexpr int PF = (GPROJ && D == 64) ? MB : 0;
+        bf16x8 ktr[PF > 0 ? PF : 1];
+#pragma unroll
+        for (int mb = 0; mb < PF; ++mb) ktr[mb] = ld_tr_operand<D>(Kc, 32 * kh, mb * 16, c16, g);
         // S^T = K Q^T and dP^T = V dO^T for this wave's 32 keys x 32 queries:
         // s[nb][kb] holds keys 4g+i of key block kb for query block nb.
         // Raise this wave's issue priority while it feeds the matrix core, so
@@ -249,7 +256,8 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
         __builtin_amdgcn_s_setprio(0);
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
-            const bf16x8 ka = ld_tr_operand<D>(Kc, 32 * kh, mb * 16, c16, g);
+            const bf16x8 ka =
+                mb < PF ? ktr[mb < PF ? mb : 0] : ld_tr_operand<D>(Kc, 32 * kh, mb * 16, c16, g);
 #pragma unroll
             for (int nb = 0; nb < 2; ++nb) {
                 accA[nb][mb] = mfma_16x16x32(ka, tf[nb], accA[nb][mb]);

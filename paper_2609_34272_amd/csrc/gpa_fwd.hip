@@ -167,11 +167,15 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
             // A wave half may not have seen a visible key yet (mnew = -inf);
             // then every z is 0 and nothing is rescaled.
             const float ms = (mnew == -INFINITY) ? 0.f : mnew;
-            // Rescale by exp2(fl32[fl32(mold - mnew) * c]): the same rule as z.
-            const float corr = fexp2((mrun[nb] - ms) * c);
-            lrun[nb] *= corr;
+            // Rescale by exp2(fl32[fl32(mold - mnew) * c]): the same rule as z;
+            // skipped when no query of the wave has a new maximum (corr is then
+            // exactly 1).
+            if (__builtin_amdgcn_ballot_w64(mnew != mrun[nb]) != 0) {
+                const float corr = fexp2((mrun[nb] - ms) * c);
+                lrun[nb] *= corr;
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb) acc[nb][mb] *= corr;
+                for (int mb = 0; mb < MB; ++mb) acc[nb][mb] *= corr;
+            }
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -351,10 +355,14 @@ __global__ __launch_bounds__(kThreads, GPA_FWD16_OCC) void fwd_sbs_q16_kernel(
         mx = xor_max(mx);
         const float mnew = fmaxf(mrun, mx);
         const float ms = (mnew == -INFINITY) ? 0.f : mnew;
-        const float corr = fexp2((mrun - ms) * c);
-        lrun *= corr;
+        // Rescale only when some query of the wave has a new maximum: otherwise
+        // corr is exactly 1 in every lane and multiplying by it changes nothing.
+        if (__builtin_amdgcn_ballot_w64(mnew != mrun) != 0) {
+            const float corr = fexp2((mrun - ms) * c);
+            lrun *= corr;
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb) acc[mb] *= corr;
+            for (int mb = 0; mb < MB; ++mb) acc[mb] *= corr;
+        }
         // pf[j]: B operand of keys 32 j .. 32 j + 31 (k-layout {4g+i, 16+4g+i}).
         bf16x8 pf[2];
 #pragma unroll
