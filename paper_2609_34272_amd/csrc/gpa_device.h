@@ -283,12 +283,17 @@ __device__ __forceinline__ float xor_sum(float v) {
 // Workgroup -> (batch*head, tile).  Workgroups are dispatched round-robin over
 // the 8 XCDs (each with its own L2), and within an XCD to whichever slots free
 // up first.  When B*H is a multiple of 8, XCD x owns heads [x*BH/8, (x+1)*BH/8)
-// so one head's tiles share an L2.  Within that set the order is rank-major:
-// every head's heaviest tile, then every head's next heaviest, ... , which makes
-// the hardware's in-order dispatch a longest-first greedy schedule for any
-// number of resident workgroups.  heavy_high selects which end is heavy: the
-// query-major causal kernels' last tiles do the most work, the key-major
-// kernels' first tiles do.
+// so one head's tiles share an L2.  Those heads are taken in groups of hg,
+// just enough heads for kGroupTiles workgroups (about twice the workgroups an
+// XCD holds at once), one group after the other: the tiles in flight then
+// stream the data of one or two heads, not of every head of the XCD (which
+// would not fit in its L2 at long sequences).  Within a group the order is
+// rank-major: every head's heaviest tile, then every head's next heaviest,
+// ... , which makes the hardware's in-order dispatch a longest-first greedy
+// schedule for any number of resident workgroups.  heavy_high selects which
+// end is heavy: the query-major causal kernels' last tiles do the most work,
+// the key-major kernels' first tiles do.
+constexpr int kGroupTiles = 128;
 __device__ __forceinline__ void map_block(int bid, int BH, int T, bool heavy_high, int* bh,
                                           int* tile) {
     int heads = BH, base = 0, li = bid;
@@ -297,8 +302,13 @@ __device__ __forceinline__ void map_block(int bid, int BH, int T, bool heavy_hig
         base = (bid & 7) * heads;
         li = bid >> 3;
     }
-    const int rank = li / heads;
-    *bh = base + (li - rank * heads);
+    const int hg = min(heads, max(1, (kGroupTiles + T - 1) / T));
+    const int group = li / (hg * T);
+    const int first = group * hg;
+    const int gs = min(hg, heads - first);  // the last group may be smaller
+    const int within = li - group * hg * T;
+    const int rank = within / gs;
+    *bh = base + first + (within - rank * gs);
     *tile = heavy_high ? (T - 1 - rank) : rank;
 }
 
