@@ -22,6 +22,12 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-I", INCLUDE, "-I", CSRC, "-Wall"]
 
 
+# Per-source scheduler choice: the backward kernels measured 2-3 % faster
+# with LLVM's iterative ILP-oriented machine scheduler (the forward was slower
+# with it, so it keeps the default).
+EXTRA = {"gpa_bwd.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"]}
+
+
 def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
@@ -33,7 +39,7 @@ def build(verbose: bool = False) -> str:
     for src in sources():
         obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
         objs.append(obj)
-        cmd = [HIPCC, *COMMON, "-c", src, "-o", obj]
+        cmd = [HIPCC, *COMMON, *EXTRA.get(os.path.basename(src), []), "-c", src, "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))
