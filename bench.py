@@ -225,6 +225,11 @@ def main():
             for m in gpa.MODES:
                 dq, dk, dv = gpa.attn_bwd(q, k, v, o, lse, u, m, w.causal, w.scale, workspace=ws[m])
                 res[m] = (o, dq, dk, dv)
+            # FA3 as the paper describes it: the historical FMA exponent rounding
+            # in the forward, then the plain backward on its O and LSE.
+            of, lf = gpa.attn_fwd_fma(q, k, v, w.causal, w.scale)
+            res["fa3_fma_plain"] = (of, *gpa.attn_bwd(q, k, v, of, lf, u, "plain", w.causal,
+                                                       w.scale, workspace=ws["plain"]))
             torch.cuda.synchronize()
             host = lambda t: t.float().cpu().numpy().astype(np.float64)  # noqa: E731
             for m, (oo, dq, dk, dv) in res.items():
