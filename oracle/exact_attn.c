@@ -156,16 +156,30 @@ static int one_head(int64_t N, int64_t d, int causal, double alpha,
  * BH heads laid out as [BH][N][d] (row-major, d innermost), LSE as [BH][N].
  * Returns 0 on success, 1 on allocation failure, 2 on bad arguments.
  */
-int oracle_attention_f64(int64_t BH, int64_t N, int64_t d, int causal, double alpha,
-                         const double* Q, const double* K, const double* V, const double* dO,
-                         double* O, double* LSE, double* dQ, double* dK, double* dV,
-                         int nthreads) {
-    if (BH < 0 || N < 0 || d < 1) return 2;
+/* nthreads > 0 runs the call on that many OpenMP threads and restores the
+ * previous setting afterwards; 0 keeps the current setting. */
+static int push_threads(int nthreads) {
 #ifdef _OPENMP
+    const int prev = omp_get_max_threads();
     if (nthreads > 0) omp_set_num_threads(nthreads);
+    return prev;
 #else
     (void)nthreads;
+    return 1;
 #endif
+}
+
+static void pop_threads(int prev) {
+#ifdef _OPENMP
+    omp_set_num_threads(prev);
+#else
+    (void)prev;
+#endif
+}
+
+static int attention_heads(int64_t BH, int64_t N, int64_t d, int causal, double alpha,
+                           const double* Q, const double* K, const double* V, const double* dO,
+                           double* O, double* LSE, double* dQ, double* dK, double* dV) {
     for (int64_t h = 0; h < BH; ++h) {
         int64_t off = h * N * d;
         if (N == 0) continue;
@@ -174,6 +188,17 @@ int oracle_attention_f64(int64_t BH, int64_t N, int64_t d, int causal, double al
             return 1;
     }
     return 0;
+}
+
+int oracle_attention_f64(int64_t BH, int64_t N, int64_t d, int causal, double alpha,
+                         const double* Q, const double* K, const double* V, const double* dO,
+                         double* O, double* LSE, double* dQ, double* dK, double* dV,
+                         int nthreads) {
+    if (BH < 0 || N < 0 || d < 1) return 2;
+    const int prev = push_threads(nthreads);
+    const int rc = attention_heads(BH, N, d, causal, alpha, Q, K, V, dO, O, LSE, dQ, dK, dV);
+    pop_threads(prev);
+    return rc;
 }
 
 /*
@@ -185,16 +210,10 @@ int oracle_attention_f64(int64_t BH, int64_t N, int64_t d, int causal, double al
  * contributions also sum over the query heads that share a KV head), added in
  * head order.  Returns 0, 1 (allocation failure) or 2 (bad arguments).
  */
-int oracle_attention_gqa_f64(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t d, int causal,
-                             double alpha, const double* Q, const double* K, const double* V,
-                             const double* dO, double* O, double* LSE, double* dQ, double* dK,
-                             double* dV, int nthreads) {
-    if (B < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || N < 0 || d < 1) return 2;
-#ifdef _OPENMP
-    if (nthreads > 0) omp_set_num_threads(nthreads);
-#else
-    (void)nthreads;
-#endif
+static int attention_gqa(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t d, int causal,
+                         double alpha, const double* Q, const double* K, const double* V,
+                         const double* dO, double* O, double* LSE, double* dQ, double* dK,
+                         double* dV) {
     const int64_t G = Hq / Hkv, hd = N * d;
     memset(dK, 0, (size_t)(B * Hkv * hd) * sizeof(double));
     memset(dV, 0, (size_t)(B * Hkv * hd) * sizeof(double));
@@ -220,6 +239,17 @@ int oracle_attention_gqa_f64(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int6
         }
     free(tk); free(tv);
     return 0;
+}
+
+int oracle_attention_gqa_f64(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t d, int causal,
+                             double alpha, const double* Q, const double* K, const double* V,
+                             const double* dO, double* O, double* LSE, double* dQ, double* dK,
+                             double* dV, int nthreads) {
+    if (B < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || N < 0 || d < 1) return 2;
+    const int prev = push_threads(nthreads);
+    const int rc = attention_gqa(B, Hq, Hkv, N, d, causal, alpha, Q, K, V, dO, O, LSE, dQ, dK, dV);
+    pop_threads(prev);
+    return rc;
 }
 
 int oracle_max_threads(void) {
