@@ -19,7 +19,9 @@ Contents
                         points, used for semantics checks (the -24 witness,
                         mode identities) and to predict error magnitudes.
   exact_varlen          exact() over packed variable-length sequences (each
-                        sequence its own attention problem).
+                        sequence its own attention problem; separate query
+                        and key lengths with the causal diagonal aligned at
+                        the end, empty rows).
   rel_l2                the paper's metric: 100 ||G_hat - G64||_2 / ||G64||_2
                         over a full tensor (appendix "Reference and metric").
 """
@@ -131,34 +133,78 @@ def _exact_gqa(lib, Q, K, V, U, causal, scale, nthreads):
     return dict(O=O, LSE=LSE, dQ=dQ, dK=dK, dV=dV)
 
 
-def exact_varlen(q, k, v, do, cu_seqlens, causal: bool, scale: float, nthreads: int = 0):
+def exact_varlen(q, k, v, do, cu_seqlens, causal: bool, scale: float, nthreads: int = 0,
+                 cu_seqlens_k=None):
     """Exact FP64 attention over packed sequences.
 
-    q, do: [Hq, total, d]; k, v: [Hkv, total, d] (Hkv dividing Hq); sequence
-    s holds tokens cu_seqlens[s] .. cu_seqlens[s+1]-1.  Attention never crosses
-    a sequence boundary, so each sequence is its own attention problem
-    (Section 3.2 with the support L_i restricted to the query's sequence): this
-    slices every sequence out and calls exact() on it.  Returns O, LSE ([Hq,
-    total]), dQ, dK, dV shaped like the inputs; rows outside every sequence
-    are zero.
+    q, do: [Hq, total_q, d]; k, v: [Hkv, total_k, d] (Hkv dividing Hq).
+    Sequence s holds queries cu_seqlens[s] .. cu_seqlens[s+1]-1 and keys
+    cu_seqlens_k[s] .. cu_seqlens_k[s+1]-1 (the same offsets when
+    cu_seqlens_k is None).  Attention never crosses a sequence boundary.  With
+    causal, query i of a sequence with nq queries and nk keys sees key j iff
+    j <= i + (nk - nq) (the causal diagonal aligned at the last query and key);
+    a query that sees no key is empty: its O and dQ are 0 and its LSE is +inf.
+
+    Each sequence is reduced to square problems of exact() (Section 3.2 with
+    the support restricted to the visible keys): with causal, the queries are
+    padded at the top with nk - nq rows of zero upstream gradient (or, when
+    nq > nk, the first nq - nk rows are the empty ones); without, the queries
+    are cut into chunks of nk rows (zero-gradient padding in the last).  Padding
+    rows have u = 0, so they contribute exactly 0 to dK and dV.  Returns O, LSE
+    ([Hq, total_q]), dQ, dK, dV shaped like the inputs.
     """
     Q, K, V, U = (as_f64(t) for t in (q, k, v, do))
-    cu = [int(x) for x in np.asarray(cu_seqlens).ravel()]
-    Hq, total, d = Q.shape
-    Hkv = K.shape[0]
-    if K.shape != (Hkv, total, d) or V.shape != K.shape or U.shape != Q.shape or Hq % Hkv:
-        raise ValueError("packed shapes: q, do [Hq, total, d]; k, v [Hkv, total, d]")
-    if cu[0] != 0 or cu[-1] != total or any(b < a for a, b in zip(cu, cu[1:])):
-        raise ValueError("cu_seqlens must start at 0, end at total and be non-decreasing")
-    out = dict(O=np.zeros_like(Q), LSE=np.zeros((Hq, total)), dQ=np.zeros_like(Q),
+    cq = [int(x) for x in np.asarray(cu_seqlens).ravel()]
+    ck = cq if cu_seqlens_k is None else [int(x) for x in np.asarray(cu_seqlens_k).ravel()]
+    Hq, tq, d = Q.shape
+    Hkv, tk = K.shape[0], K.shape[1]
+    if K.shape != (Hkv, tk, d) or V.shape != K.shape or U.shape != Q.shape or Hq % Hkv:
+        raise ValueError("packed shapes: q, do [Hq, total_q, d]; k, v [Hkv, total_k, d]")
+    for cu, tot in ((cq, tq), (ck, tk)):
+        if cu[0] != 0 or cu[-1] != tot or any(b < a for a, b in zip(cu, cu[1:])):
+            raise ValueError("offsets must start at 0, end at the total and be non-decreasing")
+    if len(cq) != len(ck):
+        raise ValueError("query and key offsets must describe the same number of sequences")
+    out = dict(O=np.zeros_like(Q), LSE=np.full((Hq, tq), np.inf), dQ=np.zeros_like(Q),
                dK=np.zeros_like(K), dV=np.zeros_like(K))
-    for a, b in zip(cu, cu[1:]):
-        if b == a:
+
+    def square(qs, us, ks, vs, causal_):
+        r = exact(qs[None], ks[None], vs[None], us[None], causal_, scale, nthreads)
+        return {n: r[n][0] for n in r}
+
+    for s in range(len(cq) - 1):
+        a, b, ka, kb = cq[s], cq[s + 1], ck[s], ck[s + 1]
+        nq, nk = b - a, kb - ka
+        if nq == 0 or nk == 0:
             continue
-        r = exact(Q[None, :, a:b], K[None, :, a:b], V[None, :, a:b], U[None, :, a:b], causal,
-                  scale, nthreads)
-        for n in out:
-            out[n][:, a:b] = r[n][0]
+        Qs, Us, Ks, Vs = Q[:, a:b], U[:, a:b], K[:, ka:kb], V[:, ka:kb]
+        if causal:
+            if nq <= nk:
+                pad = nk - nq
+                zq = np.zeros((Hq, pad, d))
+                r = square(np.concatenate([zq, Qs], 1), np.concatenate([zq, Us], 1), Ks, Vs, True)
+                rows = slice(pad, nk)
+                out["O"][:, a:b], out["LSE"][:, a:b], out["dQ"][:, a:b] = (
+                    r["O"][:, rows], r["LSE"][:, rows], r["dQ"][:, rows])
+            else:
+                first = a + (nq - nk)  # rows before it see no key
+                r = square(Q[:, first:b], U[:, first:b], Ks, Vs, True)
+                out["O"][:, first:b], out["LSE"][:, first:b], out["dQ"][:, first:b] = (
+                    r["O"], r["LSE"], r["dQ"])
+            out["dK"][:, ka:kb] += r["dK"]
+            out["dV"][:, ka:kb] += r["dV"]
+        else:
+            for c0 in range(0, nq, nk):
+                c1 = min(nq, c0 + nk)
+                pad = nk - (c1 - c0)
+                zq = np.zeros((Hq, pad, d))
+                r = square(np.concatenate([Qs[:, c0:c1], zq], 1), np.concatenate([Us[:, c0:c1], zq], 1),
+                           Ks, Vs, False)
+                rows = slice(0, c1 - c0)
+                out["O"][:, a + c0:a + c1], out["LSE"][:, a + c0:a + c1], out["dQ"][:, a + c0:a + c1] = (
+                    r["O"][:, rows], r["LSE"][:, rows], r["dQ"][:, rows])
+                out["dK"][:, ka:kb] += r["dK"]
+                out["dV"][:, ka:kb] += r["dV"]
     return out
 
 

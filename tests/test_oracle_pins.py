@@ -384,3 +384,89 @@ def test_packed_oracle_matches_masked_brute_force(causal):
     one = int(cu[2])
     assert np.array_equal(ex["O"][:, one], np.repeat(v[:, one], Hq // Hkv, axis=0))
     assert np.all(ex["dQ"][:, one] == 0.0)
+
+
+def _decimal_packed_qk(q, k, v, u, segq, loc_q, segk, loc_k, nq_of, nk_of, causal, alpha, G,
+                       dirs=None, h=None, prec=40):
+    """Brute force over separate packed query and key axes: key j is visible to
+    query i iff they belong to the same sequence s and (without causal) always,
+    (with causal) loc_k[j] <= loc_q[i] + nk_s - nq_s.  A query with no visible
+    key has O = 0 and LSE = +inf and adds nothing to L = sum O*u."""
+    ctx = decimal.Context(prec=prec)
+    D = lambda x: ctx.create_decimal(repr(float(x)))  # noqa: E731
+    Hq, Tq, d = q.shape
+    Tk = k.shape[1]
+
+    def lift(x, dx):
+        out = [[[D(x[a, i, c]) for c in range(d)] for i in range(x.shape[1])] for a in range(x.shape[0])]
+        if dx is not None:
+            out = [[[out[a][i][c] + h * D(dx[a, i, c]) for c in range(d)] for i in range(x.shape[1])]
+                   for a in range(x.shape[0])]
+        return out
+
+    dq_, dk_, dv_ = dirs if dirs is not None else (None, None, None)
+    Qd, Kd, Vd = lift(q, dq_), lift(k, dk_), lift(v, dv_)
+    a = D(alpha)
+    O = np.zeros(q.shape)
+    LSE = np.full((Hq, Tq), np.inf)
+    Ltot = D(0)
+    for hq in range(Hq):
+        hk = hq // G
+        for i in range(Tq):
+            s = segq[i]
+            vis = [j for j in range(Tk) if segk[j] == s
+                   and (not causal or loc_k[j] <= loc_q[i] + nk_of[s] - nq_of[s])]
+            if not vis:
+                continue
+            sc = [a * sum((Qd[hq][i][c] * Kd[hk][j][c] for c in range(d)), D(0)) for j in vis]
+            e = [ctx.exp(x) for x in sc]
+            Z = sum(e, D(0))
+            LSE[hq, i] = float(ctx.ln(Z))
+            for c in range(d):
+                oc = sum((e[n] * Vd[hk][j][c] for n, j in enumerate(vis)), D(0)) / Z
+                O[hq, i, c] = float(oc)
+                Ltot += oc * D(u[hq, i, c])
+    return O, LSE, Ltot
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_packed_oracle_separate_query_key_lengths(causal):
+    """exact_varlen with separate query and key offsets (causal diagonal
+    aligned at the end) against the masked brute force: sequences with more
+    keys than queries, more queries than keys (empty causal rows), no keys,
+    no queries, and equal lengths; values and the directional derivative of L."""
+    rng = np.random.default_rng(33)
+    lens = [(3, 5), (4, 2), (0, 3), (2, 0), (1, 1), (3, 3)]
+    nq = [a for a, _ in lens]
+    nk = [b for _, b in lens]
+    cq = np.concatenate([[0], np.cumsum(nq)]).astype(np.int64)
+    ck = np.concatenate([[0], np.cumsum(nk)]).astype(np.int64)
+    segq = np.repeat(np.arange(len(lens)), nq)
+    segk = np.repeat(np.arange(len(lens)), nk)
+    loc_q = np.concatenate([np.arange(n) for n in nq])
+    loc_k = np.concatenate([np.arange(n) for n in nk])
+    Tq, Tk, d, Hq, Hkv, alpha = int(cq[-1]), int(ck[-1]), 3, 2, 1, 0.7
+    q = rng.standard_normal((Hq, Tq, d)) * 1.5
+    k = rng.standard_normal((Hkv, Tk, d)) + 1.5 * rng.standard_normal(d)
+    v = rng.standard_normal((Hkv, Tk, d))
+    u = rng.standard_normal((Hq, Tq, d))
+    ex = oracle.exact_varlen(q, k, v, u, cq, causal, alpha, cu_seqlens_k=ck)
+    G = Hq // Hkv
+    O, LSE, _ = _decimal_packed_qk(q, k, v, u, segq, loc_q, segk, loc_k, nq, nk, causal, alpha, G)
+    assert np.allclose(ex["O"], O, rtol=0, atol=1e-13)
+    fin = np.isfinite(LSE)
+    assert np.array_equal(np.isfinite(ex["LSE"]), fin)
+    assert np.allclose(ex["LSE"][fin], LSE[fin], rtol=0, atol=1e-13)
+    empty = ~fin[0]
+    if causal:
+        assert empty.any(), "the (4, 2) sequence has empty causal rows"
+    assert np.all(ex["dQ"][:, empty] == 0.0) and np.all(ex["O"][:, empty] == 0.0)
+    dirs = (rng.standard_normal(q.shape), rng.standard_normal(k.shape), rng.standard_normal(v.shape))
+    hh = decimal.Decimal("1e-15")
+    _, _, Lp = _decimal_packed_qk(q, k, v, u, segq, loc_q, segk, loc_k, nq, nk, causal, alpha, G,
+                                  dirs=dirs, h=hh)
+    _, _, Lm = _decimal_packed_qk(q, k, v, u, segq, loc_q, segk, loc_k, nq, nk, causal, alpha, G,
+                                  dirs=dirs, h=-hh)
+    fd = float((Lp - Lm) / (2 * hh))
+    an = float(sum(np.sum(g * dd) for g, dd in zip((ex["dQ"], ex["dK"], ex["dV"]), dirs)))
+    assert abs(fd - an) <= 1e-10 * max(1.0, abs(an))
