@@ -185,44 +185,59 @@ gpa_status gpa_attn_bwd_gqa(const uint16_t* Q, const uint16_t* K, const uint16_t
  * packed causal layouts, Section 5; its synthetic suite covers packed
  * segments, unequal lengths, singleton and tile-boundary rows, appendix
  * "Synthetic Numerical Suite").  nseq sequences are concatenated along the
- * token axis: sequence s holds tokens [cu_seqlens[s], cu_seqlens[s+1]) and
- * attention never crosses a sequence boundary (causal: key j visible to
- * query i of the same sequence iff j <= i).  Each (sequence, query head) is
- * exactly the problem gpa_attn_fwd_gqa / gpa_attn_bwd_gqa solve for one
- * head with N = its length, with the same arithmetic and the same kernels.
- *   Layout     Q, O, dO, dQ [Hq, total, d]; K, V, dK, dV [Hkv, total, d]
+ * token axis: sequence s holds queries [cu_seqlens_q[s], cu_seqlens_q[s+1])
+ * and keys [cu_seqlens_k[s], cu_seqlens_k[s+1]), and attention never crosses
+ * a sequence boundary.  With causal, query i of a sequence with nq queries and
+ * nk keys sees key j iff j <= i + (nk - nq): the causal diagonal is aligned
+ * at the last query and key (for nq == nk, the usual j <= i).  A query that
+ * sees no key (nk == 0, or i < nq - nk under causal) is an empty row: its O
+ * and dQ are 0, its LSE is +inf, and its rho, m and lambda are 0 (the
+ * Algorithm 1 guard for m = 0).  Each (sequence, query head) with nq == nk is
+ * exactly the problem gpa_attn_fwd_gqa / gpa_attn_bwd_gqa solve for one head
+ * with N = its length, with the same arithmetic and the same kernels.
+ *   Layout     Q, O, dO, dQ [Hq, total_q, d]; K, V, dK, dV [Hkv, total_k, d]
  *              (row t of head h at (h * total + t) * d); LSE and the workspace
- *              row statistics [Hq, total].  Grouped-query heads as in the
+ *              row statistics [Hq, total_q].  Grouped-query heads as in the
  *              *_gqa entry points.
- *   cu_seqlens device int32 array of nseq + 1 offsets, read on the device:
- *              cu_seqlens[0] = 0, non-decreasing, cu_seqlens[nseq] = total,
- *              and no sequence longer than max_seqlen (a host value, which
- *              sizes the grid and the workspace).  Sequences of length 0 are
- *              allowed.  The kernels clamp every offset to [0, total] and
- *              every length to max_seqlen, so offsets that break these rules
- *              cannot make them touch memory outside the tensors; rows no
- *              sequence covers are then left unwritten and the results are
- *              unspecified.  cu_seqlens needs 4-byte alignment.
- *   Shapes     nseq >= 1, 1 <= max_seqlen <= total, Hq*total*d < 2^31,
- *              nseq*Hq*ceil(max_seqlen/64) < 2^31.
- * The workspace layout begins like gpa_attn_bwd's with [Hq, total] row
+ *   Offsets    cu_seqlens_q, cu_seqlens_k: device int32 arrays of nseq + 1
+ *              offsets, read on the device: [0] = 0, non-decreasing,
+ *              [nseq] = total_q (total_k), and no run longer than
+ *              max_seqlen_q (max_seqlen_k), host values that size the grids
+ *              and the workspace.  cu_seqlens_k NULL means cu_seqlens_q (then
+ *              total_k and max_seqlen_k must equal total_q and max_seqlen_q).
+ *              Sequences of length 0 are allowed.  The kernels clamp every
+ *              offset to [0, total] and every length to its max_seqlen, so
+ *              offsets that break these rules cannot make them touch memory
+ *              outside the tensors; rows no sequence covers are then left
+ *              unwritten and the results are unspecified.  Both arrays need
+ *              4-byte alignment and may not overlap an output.
+ *   Shapes     nseq >= 1, 1 <= max_seqlen_q <= total_q,
+ *              1 <= max_seqlen_k <= total_k, Hq*total_q*d < 2^31,
+ *              Hq*total_k*d < 2^31,
+ *              nseq*Hq*ceil(max(max_seqlen_q, max_seqlen_k)/64) < 2^31.
+ * The workspace layout begins like gpa_attn_bwd's with [Hq, total_q] row
  * statistics (D, rho, m, lambda at the offsets gpa_bwd_stats_offsets reports
- * for B = 1, H = Hq, N = total).  Errors as for the *_gqa entry points.
+ * for B = 1, H = Hq, N = total_q).  Errors as for the *_gqa entry points.
  */
 gpa_status gpa_attn_fwd_varlen(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                               uint16_t* O, float* LSE, const int32_t* cu_seqlens, int64_t nseq,
-                               int64_t total, int64_t Hq, int64_t Hkv, int64_t max_seqlen,
-                               int64_t d, int causal, float scale, void* stream);
+                               uint16_t* O, float* LSE, const int32_t* cu_seqlens_q,
+                               const int32_t* cu_seqlens_k, int64_t nseq, int64_t total_q,
+                               int64_t total_k, int64_t Hq, int64_t Hkv, int64_t max_seqlen_q,
+                               int64_t max_seqlen_k, int64_t d, int causal, float scale,
+                               void* stream);
 
-size_t gpa_attn_bwd_varlen_workspace_bytes(int64_t nseq, int64_t total, int64_t Hq, int64_t Hkv,
-                                           int64_t max_seqlen, int64_t d, int mode);
+size_t gpa_attn_bwd_varlen_workspace_bytes(int64_t nseq, int64_t total_q, int64_t total_k,
+                                           int64_t Hq, int64_t Hkv, int64_t max_seqlen_q,
+                                           int64_t max_seqlen_k, int64_t d, int mode);
 
 gpa_status gpa_attn_bwd_varlen(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                                const uint16_t* O, const float* LSE, const uint16_t* dO,
                                uint16_t* dQ, uint16_t* dK, uint16_t* dV,
-                               const int32_t* cu_seqlens, int64_t nseq, int64_t total, int64_t Hq,
-                               int64_t Hkv, int64_t max_seqlen, int64_t d, int causal, float scale,
-                               int mode, void* workspace, size_t workspace_bytes, void* stream);
+                               const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k,
+                               int64_t nseq, int64_t total_q, int64_t total_k, int64_t Hq,
+                               int64_t Hkv, int64_t max_seqlen_q, int64_t max_seqlen_k, int64_t d,
+                               int causal, float scale, int mode, void* workspace,
+                               size_t workspace_bytes, void* stream);
 
 /*
  * FP32 attention baseline (the accuracy class of the paper's "FP32 attention",

@@ -79,11 +79,11 @@ def lib():
     L.gpa_attn_bwd_gqa.argtypes = [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, I64, INT, F32,
                                    INT, P, SZ, P]
     L.gpa_attn_fwd_varlen.restype = INT
-    L.gpa_attn_fwd_varlen.argtypes = [P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, INT, F32, P]
+    L.gpa_attn_fwd_varlen.argtypes = [P] * 7 + [I64] * 8 + [INT, F32, P]
     L.gpa_attn_bwd_varlen_workspace_bytes.restype = SZ
-    L.gpa_attn_bwd_varlen_workspace_bytes.argtypes = [I64] * 6 + [INT]
+    L.gpa_attn_bwd_varlen_workspace_bytes.argtypes = [I64] * 8 + [INT]
     L.gpa_attn_bwd_varlen.restype = INT
-    L.gpa_attn_bwd_varlen.argtypes = [P] * 10 + [I64] * 6 + [INT, F32, INT, P, SZ, P]
+    L.gpa_attn_bwd_varlen.argtypes = [P] * 11 + [I64] * 8 + [INT, F32, INT, P, SZ, P]
     L.gpa_bwd_stats_offsets.restype = INT
     L.gpa_bwd_stats_offsets.argtypes = [I64, I64, I64, I64, INT] + [ctypes.POINTER(SZ)] * 4
     L.gpa_fp32_attn_workspace_bytes.restype = SZ
@@ -232,72 +232,106 @@ def attn_bwd(q, k, v, o, lse, do, mode: str = "gproj", causal: bool = True, scal
     return dq, dk, dv, stats
 
 
-def _varlen(q, k, cu_seqlens, max_seqlen):
-    """Checks of the packed layout: q [Hq, total, d], k [Hkv, total, d], int32
-    offsets on the GPU.  Returns (nseq, total, Hq, Hkv, d, max_seqlen)."""
-    if q.dim() != 3 or k.dim() != 3 or k.shape[1] != q.shape[1] or k.shape[2] != q.shape[2]:
-        raise ValueError(f"packed q [Hq, total, d] and k [Hkv, total, d] expected, got "
-                         f"{tuple(q.shape)}, {tuple(k.shape)}")
-    Hq, total, d = (int(x) for x in q.shape)
-    Hkv = int(k.shape[0])
-    if Hkv < 1 or Hq % Hkv:
-        raise ValueError(f"query heads {Hq} must be a multiple of key/value heads {Hkv}")
-    if (not cu_seqlens.is_cuda or cu_seqlens.dtype != torch.int32 or cu_seqlens.dim() != 1
-            or cu_seqlens.numel() < 2 or not cu_seqlens.is_contiguous()):
-        raise ValueError("cu_seqlens must be a contiguous 1-D int32 GPU tensor of nseq + 1 offsets")
-    return cu_seqlens.numel() - 1, total, Hq, Hkv, d, int(max_seqlen)
+def _offsets(cu, name):
+    if (not cu.is_cuda or cu.dtype != torch.int32 or cu.dim() != 1 or cu.numel() < 2
+            or not cu.is_contiguous()):
+        raise ValueError(f"{name} must be a contiguous 1-D int32 GPU tensor of nseq + 1 offsets")
 
 
-def attn_fwd_varlen(q, k, v, cu_seqlens, max_seqlen: int, causal: bool = True, scale=None):
-    """FA3-SBS forward over packed sequences.  q: bf16 [Hq, total, d]; k, v:
-    bf16 [Hkv, total, d]; cu_seqlens: int32 [nseq + 1] offsets on the GPU
-    (sequence s = tokens cu[s] .. cu[s+1]-1); max_seqlen: the longest sequence.
-    Returns O (bf16 [Hq, total, d]) and LSE (float32 [Hq, total])."""
-    nseq, total, Hq, Hkv, d, ms = _varlen(q, k, cu_seqlens, max_seqlen)
-    _need(q, "q", (Hq, total, d), torch.bfloat16)
+class _Packed:
+    """Checked packed layout: q [Hq, total_q, d], k [Hkv, total_k, d], int32
+    offsets on the GPU for each side (the key side defaults to the query
+    side's offsets and longest run)."""
+
+    def __init__(self, q, k, cu_seqlens, max_seqlen, cu_seqlens_k, max_seqlen_k):
+        if q.dim() != 3 or k.dim() != 3 or k.shape[2] != q.shape[2]:
+            raise ValueError(f"packed q [Hq, total_q, d] and k [Hkv, total_k, d] expected, got "
+                             f"{tuple(q.shape)}, {tuple(k.shape)}")
+        self.Hq, self.total_q, self.d = (int(x) for x in q.shape)
+        self.Hkv, self.total_k = int(k.shape[0]), int(k.shape[1])
+        if self.Hkv < 1 or self.Hq % self.Hkv:
+            raise ValueError(f"query heads {self.Hq} must be a multiple of key/value heads {self.Hkv}")
+        _offsets(cu_seqlens, "cu_seqlens")
+        self.cu_q = cu_seqlens
+        self.max_q = int(max_seqlen)
+        if cu_seqlens_k is None:
+            if self.total_k != self.total_q:
+                raise ValueError("k has its own token count: pass cu_seqlens_k and max_seqlen_k")
+            self.cu_k, self.max_k = cu_seqlens, self.max_q
+        else:
+            _offsets(cu_seqlens_k, "cu_seqlens_k")
+            if cu_seqlens_k.numel() != cu_seqlens.numel():
+                raise ValueError("cu_seqlens and cu_seqlens_k must describe the same number of sequences")
+            if max_seqlen_k is None:
+                raise ValueError("cu_seqlens_k needs max_seqlen_k")
+            self.cu_k, self.max_k = cu_seqlens_k, int(max_seqlen_k)
+        self.nseq = cu_seqlens.numel() - 1
+
+    def offsets(self):
+        """The C arguments from the offsets through max_seqlen_k."""
+        return (self.cu_q.data_ptr(), self.cu_k.data_ptr(), self.nseq, self.total_q, self.total_k,
+                self.Hq, self.Hkv, self.max_q, self.max_k, self.d)
+
+
+def attn_fwd_varlen(q, k, v, cu_seqlens, max_seqlen: int, causal: bool = True, scale=None,
+                    cu_seqlens_k=None, max_seqlen_k=None):
+    """FA3-SBS forward over packed sequences.  q: bf16 [Hq, total_q, d]; k, v:
+    bf16 [Hkv, total_k, d]; cu_seqlens: int32 [nseq + 1] query offsets on the
+    GPU (sequence s = queries cu[s] .. cu[s+1]-1); max_seqlen: the longest
+    query run.  cu_seqlens_k / max_seqlen_k give the key side (default: the
+    same as the queries); with causal the diagonal is aligned at the last
+    query and key, and a query that sees no key gets O = 0, LSE = +inf.
+    Returns O (bf16 [Hq, total_q, d]) and LSE (float32 [Hq, total_q])."""
+    pk = _Packed(q, k, cu_seqlens, max_seqlen, cu_seqlens_k, max_seqlen_k)
+    _need(q, "q", (pk.Hq, pk.total_q, pk.d), torch.bfloat16)
     for t, n in ((k, "k"), (v, "v")):
-        _need(t, n, (Hkv, total, d), torch.bfloat16)
+        _need(t, n, (pk.Hkv, pk.total_k, pk.d), torch.bfloat16)
     o = torch.empty_like(q)
-    lse = torch.empty((Hq, total), dtype=torch.float32, device=q.device)
+    lse = torch.empty((pk.Hq, pk.total_q), dtype=torch.float32, device=q.device)
     _check(lib().gpa_attn_fwd_varlen(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
-                                     lse.data_ptr(), cu_seqlens.data_ptr(), nseq, total, Hq, Hkv,
-                                     ms, d, int(bool(causal)), _scale(d, scale), _stream(q)))
+                                     lse.data_ptr(), *pk.offsets(), int(bool(causal)),
+                                     _scale(pk.d, scale), _stream(q)))
     return o, lse
 
 
 def attn_bwd_varlen_workspace_bytes(nseq: int, total: int, Hq: int, Hkv: int, max_seqlen: int,
-                                    d: int, mode="gproj") -> int:
+                                    d: int, mode="gproj", total_k=None, max_seqlen_k=None) -> int:
     m = MODES[mode] if isinstance(mode, str) else int(mode)
-    return int(lib().gpa_attn_bwd_varlen_workspace_bytes(nseq, total, Hq, Hkv, max_seqlen, d, m))
+    tk = total if total_k is None else int(total_k)
+    mk = max_seqlen if max_seqlen_k is None else int(max_seqlen_k)
+    return int(lib().gpa_attn_bwd_varlen_workspace_bytes(nseq, total, tk, Hq, Hkv, max_seqlen, mk,
+                                                         d, m))
 
 
 def attn_bwd_varlen(q, k, v, o, lse, do, cu_seqlens, max_seqlen: int, mode: str = "gproj",
-                    causal: bool = True, scale=None, workspace=None, return_stats: bool = False):
+                    causal: bool = True, scale=None, workspace=None, return_stats: bool = False,
+                    cu_seqlens_k=None, max_seqlen_k=None):
     """Backward over packed sequences (layouts as attn_fwd_varlen).  Returns
-    dQ, dK, dV; with return_stats=True also FP32 [Hq, total] views D, rho, m,
-    lambda into the workspace."""
-    nseq, total, Hq, Hkv, d, ms = _varlen(q, k, cu_seqlens, max_seqlen)
+    dQ, dK, dV; with return_stats=True also FP32 [Hq, total_q] views D, rho,
+    m, lambda into the workspace."""
+    pk = _Packed(q, k, cu_seqlens, max_seqlen, cu_seqlens_k, max_seqlen_k)
     for t, n in ((q, "q"), (o, "o"), (do, "do")):
-        _need(t, n, (Hq, total, d), torch.bfloat16)
+        _need(t, n, (pk.Hq, pk.total_q, pk.d), torch.bfloat16)
     for t, n in ((k, "k"), (v, "v")):
-        _need(t, n, (Hkv, total, d), torch.bfloat16)
-    _need(lse, "lse", (Hq, total), torch.float32)
+        _need(t, n, (pk.Hkv, pk.total_k, pk.d), torch.bfloat16)
+    _need(lse, "lse", (pk.Hq, pk.total_q), torch.float32)
     mcode = MODES[mode] if isinstance(mode, str) else int(mode)
-    nbytes = attn_bwd_varlen_workspace_bytes(nseq, total, Hq, Hkv, ms, d, mcode)
+    nbytes = attn_bwd_varlen_workspace_bytes(pk.nseq, pk.total_q, pk.Hq, pk.Hkv, pk.max_q, pk.d,
+                                             mcode, pk.total_k, pk.max_k)
     if workspace is None:
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     wsz = workspace.numel() * workspace.element_size()
     _check(lib().gpa_attn_bwd_varlen(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
                                      lse.data_ptr(), do.data_ptr(), dq.data_ptr(), dk.data_ptr(),
-                                     dv.data_ptr(), cu_seqlens.data_ptr(), nseq, total, Hq, Hkv, ms,
-                                     d, int(bool(causal)), _scale(d, scale), mcode,
-                                     workspace.data_ptr(), wsz, _stream(q)))
+                                     dv.data_ptr(), *pk.offsets(), int(bool(causal)),
+                                     _scale(pk.d, scale), mcode, workspace.data_ptr(), wsz,
+                                     _stream(q)))
     if not return_stats:
         return dq, dk, dv
-    offs = bwd_stats_offsets(1, Hq, total, d, mcode)
-    n = Hq * total
-    stats = {name: workspace[off:off + 4 * n].view(torch.float32).view(Hq, total)
+    offs = bwd_stats_offsets(1, pk.Hq, pk.total_q, pk.d, mcode)
+    n = pk.Hq * pk.total_q
+    stats = {name: workspace[off:off + 4 * n].view(torch.float32).view(pk.Hq, pk.total_q)
              for name, off in offs.items()}
     return dq, dk, dv, stats
 

@@ -33,18 +33,23 @@ class _Attention(torch.autograd.Function):
 
 class _AttentionVarlen(torch.autograd.Function):
     @staticmethod
-    def forward(ctx, q, k, v, cu_seqlens, max_seqlen, causal, scale, mode):
-        o, lse = attn_fwd_varlen(q, k, v, cu_seqlens, max_seqlen, causal, scale)
-        ctx.save_for_backward(q, k, v, o, lse, cu_seqlens)
+    def forward(ctx, q, k, v, cu_seqlens, max_seqlen, causal, scale, mode, cu_seqlens_k,
+                max_seqlen_k):
+        o, lse = attn_fwd_varlen(q, k, v, cu_seqlens, max_seqlen, causal, scale, cu_seqlens_k,
+                                 max_seqlen_k)
+        cu_k = cu_seqlens if cu_seqlens_k is None else cu_seqlens_k
+        ctx.save_for_backward(q, k, v, o, lse, cu_seqlens, cu_k)
         ctx.max_seqlen, ctx.causal, ctx.scale, ctx.mode = max_seqlen, causal, scale, mode
+        ctx.max_seqlen_k = max_seqlen if cu_seqlens_k is None else max_seqlen_k
         return o
 
     @staticmethod
     def backward(ctx, do):
-        q, k, v, o, lse, cu = ctx.saved_tensors
+        q, k, v, o, lse, cu, cu_k = ctx.saved_tensors
         dq, dk, dv = attn_bwd_varlen(q, k, v, o, lse, do.contiguous(), cu, ctx.max_seqlen,
-                                     ctx.mode, ctx.causal, ctx.scale)
-        return dq, dk, dv, None, None, None, None, None
+                                     ctx.mode, ctx.causal, ctx.scale, cu_seqlens_k=cu_k,
+                                     max_seqlen_k=ctx.max_seqlen_k)
+        return dq, dk, dv, None, None, None, None, None, None, None
 
 
 def attention(q, k, v, causal: bool = True, scale=None, mode: str = "gproj"):
@@ -54,7 +59,10 @@ def attention(q, k, v, causal: bool = True, scale=None, mode: str = "gproj"):
 
 
 def attention_varlen(q, k, v, cu_seqlens, max_seqlen: int, causal: bool = True, scale=None,
-                     mode: str = "gproj"):
-    """Differentiable attention over packed sequences: q [Hq, total, d], k, v
-    [Hkv, total, d], int32 offsets cu_seqlens [nseq + 1] -> O [Hq, total, d]."""
-    return _AttentionVarlen.apply(q, k, v, cu_seqlens, int(max_seqlen), bool(causal), scale, mode)
+                     mode: str = "gproj", cu_seqlens_k=None, max_seqlen_k=None):
+    """Differentiable attention over packed sequences: q [Hq, total_q, d], k, v
+    [Hkv, total_k, d], int32 query offsets cu_seqlens [nseq + 1] (key offsets
+    cu_seqlens_k, default the same) -> O [Hq, total_q, d]."""
+    mk = None if max_seqlen_k is None else int(max_seqlen_k)
+    return _AttentionVarlen.apply(q, k, v, cu_seqlens, int(max_seqlen), bool(causal), scale, mode,
+                                  cu_seqlens_k, mk)

@@ -119,13 +119,14 @@ struct BwdLayout {
 // pass stages with the tile; then (gproj mode only) the BF16 tensor
 // z = BF16(lambda q), shaped like Q, that the key correction contracts; then,
 // for grouped-query attention (Hq > Hkv) only, the FP32 per-query-head
-// contributions to dK and dV (shaped like Q) that the group sum adds.
-BwdLayout bwd_layout_rows(size_t qrows, size_t problems, int64_t Nmax, int64_t d, int mode,
-                          bool grouped) {
+// contributions to dK and dV (Hq heads over the key rows) that the group sum
+// adds.
+BwdLayout bwd_layout_rows(size_t qrows, size_t krows, size_t problems, int64_t Nmax, int64_t d,
+                          int mode, bool grouped) {
     const size_t row = round_up(qrows * sizeof(float));
     const size_t T = (size_t)(Nmax + 63) / 64;
     const size_t tstats = round_up(problems * T * 128 * sizeof(float));
-    const size_t part = grouped ? round_up(qrows * (size_t)d * sizeof(float)) : 0;
+    const size_t part = grouped ? round_up(krows * (size_t)d * sizeof(float)) : 0;
     BwdLayout L;
     L.D = 0;
     L.rho = row;
@@ -140,16 +141,18 @@ BwdLayout bwd_layout_rows(size_t qrows, size_t problems, int64_t Nmax, int64_t d
 }
 
 BwdLayout bwd_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t N, int64_t d, int mode) {
-    return bwd_layout_rows((size_t)B * Hq * N, (size_t)B * Hq, N, d, mode, Hq > Hkv);
+    const size_t rows = (size_t)B * Hq * N;
+    return bwd_layout_rows(rows, rows, (size_t)B * Hq, N, d, mode, Hq > Hkv);
 }
 
 // Enqueue the backward passes once the arguments are validated: the
 // query-major pass, the key-major pass and, for grouped-query attention, the
-// group sum of the per-query-head dK, dV contributions.  qrows is the number
-// of query-head rows (the extent of the group-sum partials).
+// group sum of the per-query-head dK, dV contributions.  krows is the number
+// of query-head rows over the keys (Hq x key rows: the extent of the
+// group-sum partials).
 gpa_status run_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, const uint16_t* O,
                    const float* LSE, const uint16_t* dO, uint16_t* dQ, uint16_t* dK, uint16_t* dV,
-                   const gpa::Shape& sh, const BwdLayout& L, size_t qrows, int mode,
+                   const gpa::Shape& sh, const BwdLayout& L, size_t krows, int mode,
                    void* workspace, hipStream_t st) {
     char* ws = (char*)workspace;
     float* Drow = (float*)(ws + L.D);
@@ -177,10 +180,10 @@ gpa_status run_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, cons
                  "bwd_dkdv");
     if (s != GPA_OK || sh.G == 1) return s;
     // The group sum sees the partials as G consecutive query heads of
-    // qrows / Hq rows each per key/value head.
+    // krows / Hq key rows each per key/value head.
     gpa::Shape gs = sh;
     gs.BH = sh.cu ? sh.Hq : sh.BH;
-    gs.N = (int)(qrows / (size_t)gs.BH);
+    gs.N = (int)(krows / (size_t)gs.BH);
     return launched(timed(gpa::kKGroupSum, st,
                           [&] { return gpa::launch_bwd_group_sum(dkp, dvp, dK, dV, gs, st); }),
                     "group_sum");
@@ -193,40 +196,65 @@ gpa_status check_heads(int64_t Hq, int64_t Hkv) {
     return GPA_OK;
 }
 
-// Packed variable-length sequences.
-gpa_status check_varlen(const int32_t* cu, int64_t nseq, int64_t total, int64_t Hq, int64_t Hkv,
-                        int64_t max_seqlen, int64_t d, float scale) {
-    if (nseq < 1 || total < 1 || max_seqlen < 1 || max_seqlen > total)
+// Packed variable-length sequences: the query side and the key side each
+// have offsets, a total and a longest run.  Key offsets NULL means the query
+// offsets, which asks for the same total and longest run.
+struct Varlen {
+    const int32_t* cu_q;
+    const int32_t* cu_k;
+    int64_t nseq, total_q, total_k, Hq, Hkv, max_q, max_k, d;
+};
+
+gpa_status check_varlen(const Varlen& v, float scale) {
+    if (v.nseq < 1 || v.total_q < 1 || v.max_q < 1 || v.max_q > v.total_q)
         return fail(GPA_EINVAL,
-                    "need nseq >= 1, total >= 1 and 1 <= max_seqlen <= total (got %lld, %lld, %lld)",
-                    (long long)nseq, (long long)total, (long long)max_seqlen);
-    gpa_status s = check_shape(1, Hq, total, d, scale);
+                    "need nseq >= 1, total_q >= 1 and 1 <= max_seqlen_q <= total_q "
+                    "(got %lld, %lld, %lld)",
+                    (long long)v.nseq, (long long)v.total_q, (long long)v.max_q);
+    if (v.total_k < 1 || v.max_k < 1 || v.max_k > v.total_k)
+        return fail(GPA_EINVAL, "need total_k >= 1 and 1 <= max_seqlen_k <= total_k (got %lld, %lld)",
+                    (long long)v.total_k, (long long)v.max_k);
+    if (v.cu_k == v.cu_q && (v.total_k != v.total_q || v.max_k != v.max_q))
+        return fail(GPA_EINVAL, "shared offsets need total_k == total_q and max_seqlen_k == max_seqlen_q");
+    gpa_status s = check_shape(1, v.Hq, v.total_q, v.d, scale);
     if (s != GPA_OK) return s;
-    if ((s = check_heads(Hq, Hkv)) != GPA_OK) return s;
-    if (!cu) return fail(GPA_EINVAL, "cu_seqlens is NULL");
-    if ((uintptr_t)cu % 4) return fail(GPA_EINVAL, "cu_seqlens is not 4-byte aligned");
-    const double grid = (double)nseq * (double)Hq * (double)((max_seqlen + 63) / 64);
-    if (grid >= 2147483648.0 || (double)nseq * Hq >= 2147483648.0)
+    if ((s = check_shape(1, v.Hq, v.total_k, v.d, scale)) != GPA_OK) return s;
+    if ((s = check_heads(v.Hq, v.Hkv)) != GPA_OK) return s;
+    if (!v.cu_q) return fail(GPA_EINVAL, "cu_seqlens_q is NULL");
+    if ((uintptr_t)v.cu_q % 4 || (uintptr_t)v.cu_k % 4)
+        return fail(GPA_EINVAL, "sequence offsets are not 4-byte aligned");
+    const int64_t longest = v.max_q > v.max_k ? v.max_q : v.max_k;
+    const double grid = (double)v.nseq * (double)v.Hq * (double)((longest + 63) / 64);
+    if (grid >= 2147483648.0 || (double)v.nseq * v.Hq >= 2147483648.0)
         return fail(GPA_EINVAL, "nseq * Hq * ceil(max_seqlen / 64) = %.0f exceeds 2^31 - 1", grid);
     return GPA_OK;
 }
 
 // The sequence offsets are an input: no output may overlap them.
-gpa_status check_cu_overlap(const int32_t* cu, int64_t nseq, const std::vector<Buf>& outs) {
-    const Buf c{cu, 4 * (size_t)(nseq + 1), "cu_seqlens"};
+gpa_status check_cu_overlap(const Varlen& v, const std::vector<Buf>& outs) {
+    const Buf c[2] = {{v.cu_q, 4 * (size_t)(v.nseq + 1), "cu_seqlens_q"},
+                      {v.cu_k, 4 * (size_t)(v.nseq + 1), "cu_seqlens_k"}};
     for (const Buf& b : outs)
-        if (overlap(b, c)) return fail(GPA_EINVAL, "%s overlaps cu_seqlens", b.name);
+        for (const Buf& cb : c)
+            if (overlap(b, cb)) return fail(GPA_EINVAL, "%s overlaps %s", b.name, cb.name);
     return GPA_OK;
 }
 
-gpa::Shape varlen_shape(const int32_t* cu, int64_t nseq, int64_t total, int64_t Hq, int64_t Hkv,
-                        int64_t max_seqlen, int64_t d, int causal, float scale) {
-    gpa::Shape sh{(int)(nseq * Hq), (int)max_seqlen, (int)d, causal ? 1 : 0, scale,
-                  (int)(Hq / Hkv)};
-    sh.cu = cu;
-    sh.Hq = (int)Hq;
-    sh.total = (int)total;
+gpa::Shape varlen_shape(const Varlen& v, int causal, float scale) {
+    gpa::Shape sh{(int)(v.nseq * v.Hq), (int)v.max_q, (int)v.d, causal ? 1 : 0, scale,
+                  (int)(v.Hq / v.Hkv)};
+    sh.cu = v.cu_q;
+    sh.Hq = (int)v.Hq;
+    sh.total = (int)v.total_q;
+    sh.cu_k = v.cu_k;
+    sh.total_k = (int)v.total_k;
+    sh.Nk = (int)v.max_k;
     return sh;
+}
+
+BwdLayout varlen_layout(const Varlen& v, int mode) {
+    return bwd_layout_rows((size_t)v.Hq * v.total_q, (size_t)v.Hq * v.total_k,
+                           (size_t)v.nseq * v.Hq, v.max_q, v.d, mode, v.Hq > v.Hkv);
 }
 }  // namespace
 
@@ -347,64 +375,74 @@ gpa_status gpa_attn_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
 
 
 gpa_status gpa_attn_fwd_varlen(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                               uint16_t* O, float* LSE, const int32_t* cu_seqlens, int64_t nseq,
-                               int64_t total, int64_t Hq, int64_t Hkv, int64_t max_seqlen,
-                               int64_t d, int causal, float scale, void* stream) {
-    gpa_status s = check_varlen(cu_seqlens, nseq, total, Hq, Hkv, max_seqlen, d, scale);
+                               uint16_t* O, float* LSE, const int32_t* cu_seqlens_q,
+                               const int32_t* cu_seqlens_k, int64_t nseq, int64_t total_q,
+                               int64_t total_k, int64_t Hq, int64_t Hkv, int64_t max_seqlen_q,
+                               int64_t max_seqlen_k, int64_t d, int causal, float scale,
+                               void* stream) {
+    const Varlen v{cu_seqlens_q, cu_seqlens_k ? cu_seqlens_k : cu_seqlens_q, nseq, total_q,
+                   total_k, Hq, Hkv, max_seqlen_q, max_seqlen_k, d};
+    gpa_status s = check_varlen(v, scale);
     if (s != GPA_OK) return s;
-    const size_t tq = (size_t)Hq * total * d * 2, tkv = (size_t)Hkv * total * d * 2;
-    const size_t lb = (size_t)Hq * total * 4;
-    s = check_ptrs({{Q, tq, "Q"}, {K, tkv, "K"}, {V, tkv, "V"}}, {{O, tq, "O"}, {LSE, lb, "LSE"}});
+    const size_t tq = (size_t)Hq * total_q * d * 2, tkv = (size_t)Hkv * total_k * d * 2;
+    const size_t lb = (size_t)Hq * total_q * 4;
+    const std::vector<Buf> outs = {{O, tq, "O"}, {LSE, lb, "LSE"}};
+    s = check_ptrs({{Q, tq, "Q"}, {K, tkv, "K"}, {V, tkv, "V"}}, outs);
     if (s != GPA_OK) return s;
-    if ((s = check_cu_overlap(cu_seqlens, nseq, {{O, tq, "O"}, {LSE, lb, "LSE"}})) != GPA_OK)
-        return s;
-    const gpa::Shape sh = varlen_shape(cu_seqlens, nseq, total, Hq, Hkv, max_seqlen, d, causal, scale);
+    if ((s = check_cu_overlap(v, outs)) != GPA_OK) return s;
+    const gpa::Shape sh = varlen_shape(v, causal, scale);
     hipStream_t st = (hipStream_t)stream;
     return launched(timed(gpa::kKFwd, st, [&] { return gpa::launch_fwd(Q, K, V, O, LSE, sh, st); }),
                     "fwd_sbs");
 }
 
-size_t gpa_attn_bwd_varlen_workspace_bytes(int64_t nseq, int64_t total, int64_t Hq, int64_t Hkv,
-                                           int64_t max_seqlen, int64_t d, int mode) {
+size_t gpa_attn_bwd_varlen_workspace_bytes(int64_t nseq, int64_t total_q, int64_t total_k,
+                                           int64_t Hq, int64_t Hkv, int64_t max_seqlen_q,
+                                           int64_t max_seqlen_k, int64_t d, int mode) {
     if (mode < 0 || mode > 2) return 0;
-    if (nseq < 1 || total < 1 || max_seqlen < 1 || max_seqlen > total) return 0;
+    if (nseq < 1 || total_q < 1 || max_seqlen_q < 1 || max_seqlen_q > total_q) return 0;
+    if (total_k < 1 || max_seqlen_k < 1 || max_seqlen_k > total_k) return 0;
     if (Hq < 1 || Hkv < 1 || Hq % Hkv || (d != 64 && d != 128)) return 0;
-    if ((double)Hq * total * d >= 2147483648.0) return 0;
-    if ((double)nseq * Hq * (double)((max_seqlen + 63) / 64) >= 2147483648.0) return 0;
-    return bwd_layout_rows((size_t)Hq * total, (size_t)nseq * Hq, max_seqlen, d, mode, Hq > Hkv)
-        .total;
+    if ((double)Hq * total_q * d >= 2147483648.0 || (double)Hq * total_k * d >= 2147483648.0)
+        return 0;
+    const int64_t longest = max_seqlen_q > max_seqlen_k ? max_seqlen_q : max_seqlen_k;
+    if ((double)nseq * Hq * (double)((longest + 63) / 64) >= 2147483648.0) return 0;
+    const Varlen v{nullptr, nullptr, nseq, total_q, total_k, Hq, Hkv, max_seqlen_q, max_seqlen_k, d};
+    return varlen_layout(v, mode).total;
 }
 
 gpa_status gpa_attn_bwd_varlen(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                                const uint16_t* O, const float* LSE, const uint16_t* dO,
                                uint16_t* dQ, uint16_t* dK, uint16_t* dV,
-                               const int32_t* cu_seqlens, int64_t nseq, int64_t total, int64_t Hq,
-                               int64_t Hkv, int64_t max_seqlen, int64_t d, int causal, float scale,
-                               int mode, void* workspace, size_t workspace_bytes, void* stream) {
-    gpa_status s = check_varlen(cu_seqlens, nseq, total, Hq, Hkv, max_seqlen, d, scale);
+                               const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k,
+                               int64_t nseq, int64_t total_q, int64_t total_k, int64_t Hq,
+                               int64_t Hkv, int64_t max_seqlen_q, int64_t max_seqlen_k, int64_t d,
+                               int causal, float scale, int mode, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+    const Varlen v{cu_seqlens_q, cu_seqlens_k ? cu_seqlens_k : cu_seqlens_q, nseq, total_q,
+                   total_k, Hq, Hkv, max_seqlen_q, max_seqlen_k, d};
+    gpa_status s = check_varlen(v, scale);
     if (s != GPA_OK) return s;
     if (mode < 0 || mode > 2) return fail(GPA_EINVAL, "mode %d is not 0, 1 or 2", mode);
-    const size_t need =
-        gpa_attn_bwd_varlen_workspace_bytes(nseq, total, Hq, Hkv, max_seqlen, d, mode);
+    const size_t need = gpa_attn_bwd_varlen_workspace_bytes(nseq, total_q, total_k, Hq, Hkv,
+                                                            max_seqlen_q, max_seqlen_k, d, mode);
     if (!workspace || workspace_bytes < need)
         return fail(GPA_EWORKSPACE, "workspace %p of %zu bytes; %zu needed", workspace,
                     workspace_bytes, need);
     if ((uintptr_t)workspace % kAlign)
         return fail(GPA_EWORKSPACE, "workspace is not %zu-byte aligned", kAlign);
-    const size_t tq = (size_t)Hq * total * d * 2, tkv = (size_t)Hkv * total * d * 2;
-    const size_t lb = (size_t)Hq * total * 4;
+    const size_t tq = (size_t)Hq * total_q * d * 2, tkv = (size_t)Hkv * total_k * d * 2;
+    const size_t lb = (size_t)Hq * total_q * 4;
     const std::vector<Buf> outs = {
         {dQ, tq, "dQ"}, {dK, tkv, "dK"}, {dV, tkv, "dV"}, {workspace, need, "workspace"}};
     s = check_ptrs({{Q, tq, "Q"}, {K, tkv, "K"}, {V, tkv, "V"}, {O, tq, "O"}, {LSE, lb, "LSE"},
                     {dO, tq, "dO"}},
                    outs);
     if (s != GPA_OK) return s;
-    if ((s = check_cu_overlap(cu_seqlens, nseq, outs)) != GPA_OK) return s;
-    const gpa::Shape sh = varlen_shape(cu_seqlens, nseq, total, Hq, Hkv, max_seqlen, d, causal, scale);
-    const BwdLayout L =
-        bwd_layout_rows((size_t)Hq * total, (size_t)nseq * Hq, max_seqlen, d, mode, Hq > Hkv);
-    return run_bwd(Q, K, V, O, LSE, dO, dQ, dK, dV, sh, L, (size_t)Hq * total, mode, workspace,
-                   (hipStream_t)stream);
+    if ((s = check_cu_overlap(v, outs)) != GPA_OK) return s;
+    const gpa::Shape sh = varlen_shape(v, causal, scale);
+    return run_bwd(Q, K, V, O, LSE, dO, dQ, dK, dV, sh, varlen_layout(v, mode),
+                   (size_t)Hq * total_k, mode, workspace, (hipStream_t)stream);
 }
 
 size_t gpa_fp32_attn_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d) {

@@ -77,8 +77,8 @@ __device__ __forceinline__ void pair_reduce(float (&v)[NV], float* scratch, int 
 // tail masks (only diagonal and tail tiles need them).
 template <bool MASK>
 __device__ __forceinline__ void dq_probs(const f32x4 (&s)[2], const f32x4 (&dp)[2], float c,
-                                         float lse2, float Di, int key0, int g, int qrow, int N,
-                                         int causal, bf16x8& tf, bf16x8& rf) {
+                                         float lse2, float Di, int key0, int g, int qrow, int Nk,
+                                         int causal, int off, bf16x8& tf, bf16x8& rf) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -86,7 +86,7 @@ __device__ __forceinline__ void dq_probs(const f32x4 (&s)[2], const f32x4 (&dp)[
             float P = fexp2(fmaf(s[kb][i], c, -lse2));
             if constexpr (MASK) {
                 const int key = key0 + kb * 16 + 4 * g + i;
-                const bool ok = key < N && (!causal || key <= qrow);
+                const bool ok = key < Nk && (!causal || key <= qrow + off);
                 P = ok ? P : 0.f;
             }
             tf[kb * 4 + i] = to_bf16(P * (dp[kb][i] - Di));
@@ -102,7 +102,8 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     float* __restrict__ TS, uint16_t* __restrict__ dQ,
     float* __restrict__ rho_out, float* __restrict__ m_out, float* __restrict__ lam_out,
     uint16_t* __restrict__ Zout, int BH, int Nmax, int causal, float scale, int G,
-    const int* __restrict__ cu, int Hq, int total) {
+    const int* __restrict__ cu, int Hq, int total, const int* __restrict__ cu_k, int total_k,
+    int Nkmax) {
     constexpr int MB = D / 16;  // 16-column blocks of d
     constexpr int KC = D / 32;  // 32-wide k chunks of d
     constexpr int PER_NB = 2 * MB * 4 + 2;  // partial A, B (interleaved) and rho, m
@@ -117,10 +118,10 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     const int T = (Nmax + kTile - 1) / kTile;  // tiles of the longest problem
     int bh, tile;
     map_block(blockIdx.x, BH, T, causal != 0, &bh, &tile);
-    const SeqRows sr = seq_rows(cu, bh, Nmax, G, Hq, total);
-    const int N = sr.n;
+    const SeqRows sr = seq_rows(cu, cu_k, bh, Nmax, Nkmax, G, Hq, total, total_k);
+    const int N = sr.nq, Nk = sr.nk;
     if (tile * kTile >= N) return;  // a shorter sequence has no such tile
-    const int Tn = (N + kTile - 1) / kTile;
+    const int off = Nk - N;           // causal: query i sees key j iff j <= i + off
     const size_t hoff = sr.q0 * D;    // query head
     const size_t kvoff = sr.kv0 * D;  // its key/value head
     const size_t soff = sr.q0;
@@ -177,11 +178,12 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
         accM[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
 
-    const int nkv = causal ? min(Tn, tile + 1) : Tn;
-    // Only the last key tile can need masks: the diagonal tile (causal) or the
-    // key tail (N not a multiple of the tile).  Query rows beyond N need none
-    // (their P is 0 and they are not stored).
-    const int nplain = (causal || (N % kTile)) ? nkv - 1 : nkv;
+    // Only the last one or two key tiles need masks (the causal diagonal, the
+    // key tail).  Query rows beyond N need none (their P is 0 and they are not
+    // stored), nor do queries that see no key (the forward gave them
+    // LSE = +inf).
+    const KeyRange kr = key_range(tile, Nk, off, causal);
+    const int nkv = kr.nkv, nplain = kr.nplain;
 
     TileDma<D> dma;
     dma.init(lane, wave);
@@ -191,7 +193,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     auto fill_piece = [&](uint16_t* slot, int kt, int j) {
         if (j < FILL_VM) {
             const int t = j / TileDma<D>::CALLS, k = j % TileDma<D>::CALLS;
-            dma.load_call(t ? V + kvoff : K + kvoff, slot + t * TILE_E, kt * kTile, N, kt < nkv, k);
+            dma.load_call(t ? V + kvoff : K + kvoff, slot + t * TILE_E, kt * kTile, Nk, kt < nkv, k);
         }
     };
     // The register operands above must have arrived before the first fill: the
@@ -250,7 +252,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb)
             dq_probs<MASK>(s[nb], dp[nb], c, lse2[nb], Di[nb], k0 + 32 * kh, g,
-                           q0w + nb * 16 + c16, N, causal, tf[nb], rf[nb]);
+                           q0w + nb * 16 + c16, Nk, causal, off, tf[nb], rf[nb]);
         // A^T[d][query] += K^T[d][key] t^T[key][query] (and B^T with r); the
         // row sums rho, m come from a constant ones operand.
         __builtin_amdgcn_s_setprio(0);
@@ -278,21 +280,21 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     };
     const std::false_type plain;
     const std::true_type masked;
-    // Tile t lives in slot t mod 3; only the last tile can need masks.
+    // Tile t lives in slot t mod 3; only the last one or two tiles need masks.
     int kt = 0;
     for (; kt < nplain; kt += 3) {
         step(plain, kt, S0, S2);
         if (kt + 1 < nplain) step(plain, kt + 1, S1, S0);
         if (kt + 2 < nplain) step(plain, kt + 2, S2, S1);
     }
-    if (nplain < nkv) {
-        const int r = nplain % 3;
+    for (kt = nplain; kt < nkv; ++kt) {
+        const int r = kt % 3;
         if (r == 0)
-            step(masked, nplain, S0, S2);
+            step(masked, kt, S0, S2);
         else if (r == 1)
-            step(masked, nplain, S1, S0);
+            step(masked, kt, S1, S0);
         else
-            step(masked, nplain, S2, S1);
+            step(masked, kt, S2, S1);
     }
     // The zero fills issued by the last steps must land before slot 0 is
     // reused for the reduction.
@@ -379,16 +381,18 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
 // ----------------------------------------------------------- key-major pass
 // P, r, t of one 16-key x 16-query block: s, dp hold queries 4g+i of the
 // block for this lane's key; they fill half `half` of the B operands tf, rf.
-// Query rows beyond N have log2-LSE = +inf (P = 0); key rows beyond N are
-// never stored; so only the causal diagonal needs a mask.
+// Query rows beyond N, and queries that see no key, have log2-LSE = +inf
+// (P = 0); key rows beyond the key count are never stored; so only the causal
+// diagonal needs a mask: key krow is visible to query qrow iff
+// krow <= qrow + off.
 template <bool MASK>
 __device__ __forceinline__ void dkdv_probs(const f32x4& s, const f32x4& dp, const f32x4& l2,
                                            const f32x4& dd, float c, int qb, int g, int krow,
-                                           int half, bf16x8& tf, bf16x8& rf) {
+                                           int off, int half, bf16x8& tf, bf16x8& rf) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         float P = fexp2(fmaf(s[i], c, -l2[i]));
-        if constexpr (MASK) P = (krow <= qb + 4 * g + i) ? P : 0.f;
+        if constexpr (MASK) P = (krow <= qb + 4 * g + i + off) ? P : 0.f;
         tf[half * 4 + i] = to_bf16(P * (dp[i] - dd[i]));
         rf[half * 4 + i] = to_bf16(P);
     }
@@ -400,7 +404,8 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
     const float* __restrict__ TS, const uint16_t* __restrict__ Z, uint16_t* __restrict__ dK,
     uint16_t* __restrict__ dV, float* __restrict__ dKp, float* __restrict__ dVp, int BH, int Nmax,
-    int causal, float scale, int G, const int* __restrict__ cu, int Hq, int total) {
+    int causal, float scale, int G, const int* __restrict__ cu, int Hq, int total,
+    const int* __restrict__ cu_k, int total_k, int Nkmax) {
     constexpr int MB = D / 16;
     constexpr int KC = D / 32;
     constexpr int NT = GPROJ ? 3 : 2;  // staged tensors: Q, dO (and Z = BF16(lambda Q))
@@ -418,16 +423,19 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     __shared__ __attribute__((aligned(16))) uint16_t B1[SLOT_E];
     __shared__ __attribute__((aligned(16))) uint16_t B2[SLOT_E];
 
-    const int Tmax = (Nmax + kTile - 1) / kTile;  // tiles of the longest problem
+    const int Tq = (Nmax + kTile - 1) / kTile;   // query tiles of the longest problem
+    const int Tk = (Nkmax + kTile - 1) / kTile;  // key tiles of the longest problem
     int bh, tile;
-    map_block(blockIdx.x, BH, Tmax, false, &bh, &tile);
-    const SeqRows sr = seq_rows(cu, bh, Nmax, G, Hq, total);
-    const int N = sr.n;
-    if (tile * kTile >= N) return;  // a shorter sequence has no such tile
+    map_block(blockIdx.x, BH, Tk, false, &bh, &tile);
+    const SeqRows sr = seq_rows(cu, cu_k, bh, Nmax, Nkmax, G, Hq, total, total_k);
+    const int N = sr.nq, Nk = sr.nk;
+    if (tile * kTile >= Nk) return;  // a shorter sequence has no such tile
     const int T = (N + kTile - 1) / kTile;
-    const size_t hoff = sr.q0 * D;    // query head: Q, dO, z, partials
+    const int off = Nk - N;           // causal: query i sees key j iff j <= i + off
+    const size_t hoff = sr.q0 * D;    // query head: Q, dO, z
     const size_t kvoff = sr.kv0 * D;  // its key/value head: K, V, dK, dV
-    const float* tsh = TS + (size_t)bh * Tmax * kStatFloats;
+    const size_t poff = sr.p0 * D;    // this query head's partials over the key rows
+    const float* tsh = TS + (size_t)bh * Tq * kStatFloats;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -437,8 +445,8 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     const int k0w = tile * kTile + 32 * kh;
 
     // K^T and V^T as B operands: column = this lane's key of block kb, k = d.
-    // Rows beyond N load as zero.
-    const uint32_t tbytes = (uint32_t)N * (2 * D);
+    // Rows beyond the key count load as zero.
+    const uint32_t tbytes = (uint32_t)Nk * (2 * D);
     const rsrc_t rk = make_rsrc(K + kvoff, tbytes);
     const rsrc_t rv = make_rsrc(V + kvoff, tbytes);
     bf16x8 kf[2][KC], vf[2][KC];
@@ -464,7 +472,11 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
         for (int mb = 0; mb < (GPROJ ? MB : 1); ++mb) accC[kb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
 
-    const int qt0 = causal ? tile : 0;
+    // The first query tile that sees a key of this tile.  The causal boundary
+    // crosses at most the first two query tiles; without causal no query is
+    // masked (a mask offset no row reaches).
+    const int qt0 = causal ? max(0, floor_div(tile * kTile - off, kTile)) : 0;
+    const int moff = causal ? off : (1 << 30);
     const uint16_t* src[NT];
     src[0] = Q + hoff;
     src[1] = dO + hoff;
@@ -564,7 +576,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
                     dpv = mfma_16x16x32(ua[kc], vf[kb][kc], dpv);
                 }
                 dkdv_probs<MASK>(sv, dpv, l2[mq], dd[mq], c, q0 + 32 * qh + mq * 16, g,
-                                 k0w + kb * 16 + c16, mq, tf[kb], rf[kb]);
+                                 k0w + kb * 16 + c16, moff, mq, tf[kb], rf[kb]);
                 fill_piece(nxt2, qt + 2, AT_START + mq * 2 + kb);
             }
         }
@@ -590,16 +602,14 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     };
     const std::false_type plain;
     const std::true_type masked;
-    // Tile t lives in slot (t - qt0) mod 3.  Causal: only the diagonal tile
-    // (the first one) needs a mask.
-    if (causal)
-        step(masked, qt0, B0, B2);
-    else
-        step(plain, qt0, B0, B2);
-    for (int qt = qt0 + 1; qt < T; qt += 3) {
-        step(plain, qt, B1, B0);
-        if (qt + 1 < T) step(plain, qt + 1, B2, B1);
-        if (qt + 2 < T) step(plain, qt + 2, B0, B2);
+    // Tile t lives in slot (t - qt0) mod 3; the first two steps take the mask.
+    // A key tile that no query sees (qt0 >= T) takes no step and stores zeros.
+    if (qt0 < T) step(masked, qt0, B0, B2);
+    if (qt0 + 1 < T) step(masked, qt0 + 1, B1, B0);
+    for (int qt = qt0 + 2; qt < T; qt += 3) {
+        step(plain, qt, B2, B1);
+        if (qt + 1 < T) step(plain, qt + 1, B0, B2);
+        if (qt + 2 < T) step(plain, qt + 2, B1, B0);
     }
     // The zero fills issued by the last steps must land before B0 is reused
     // for the reduction.
@@ -628,11 +638,11 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
         const int krow = k0w + kb * 16 + c16;
-        if (krow >= N) continue;
+        if (krow >= Nk) continue;
         if (G > 1) {
             // This query head's FP32 contributions; the group sum casts them.
-            float* vp = dVp + hoff + (size_t)krow * D;
-            float* kp = dKp + hoff + (size_t)krow * D;
+            float* vp = dVp + poff + (size_t)krow * D;
+            float* kp = dKp + poff + (size_t)krow * D;
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb) {
                 f32x4 dv, dk;
@@ -707,11 +717,13 @@ hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V
                          float* TS, uint16_t* dQ, float* rho, float* msum, float* lambda,
                          uint16_t* Z, int mode, const Shape& s, hipStream_t st) {
     const int T = (s.N + kTile - 1) / kTile;
+    const int Nk = s.Nk > 0 ? s.Nk : s.N;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
 #define GPA_DQ(DD, GP, WZ)                                                                   \
     bwd_dq_kernel<DD, GP, WZ><<<grid, block, 0, st>>>(Q, K, V, O, dO, LSE, Drow, TS, dQ, rho, \
                                                       msum, lambda, Z, s.BH, s.N, s.causal,  \
-                                                      s.scale, s.G, s.cu, s.Hq, s.total)
+                                                      s.scale, s.G, s.cu, s.Hq, s.total,     \
+                                                      s.cu_k, s.total_k, Nk)
     if (s.d == 64) {
         if (mode == 2) GPA_DQ(64, true, true);
         else if (mode == 1) GPA_DQ(64, true, false);
@@ -729,13 +741,14 @@ hipError_t launch_bwd_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t*
                            const uint16_t* dO, const float* TS, const uint16_t* Z,
                            uint16_t* dK, uint16_t* dV, float* dKp, float* dVp, int mode,
                            const Shape& s, hipStream_t st) {
-    const int T = (s.N + kTile - 1) / kTile;
-    dim3 grid((unsigned)(s.BH * T)), block(kThreads);
+    const int Nk = s.Nk > 0 ? s.Nk : s.N;
+    const int Tk = (Nk + kTile - 1) / kTile;
+    dim3 grid((unsigned)(s.BH * Tk)), block(kThreads);
     const bool gp = mode == 2;
 #define GPA_DKDV(DD, GP)                                                             \
     bwd_dkdv_kernel<DD, GP><<<grid, block, 0, st>>>(Q, K, V, dO, TS, Z, dK, dV, dKp, dVp, \
                                                     s.BH, s.N, s.causal, s.scale, s.G, s.cu, \
-                                                    s.Hq, s.total)
+                                                    s.Hq, s.total, s.cu_k, s.total_k, Nk)
     if (s.d == 64) {
         if (gp) GPA_DKDV(64, true); else GPA_DKDV(64, false);
     } else {

@@ -312,24 +312,52 @@ __device__ __forceinline__ void map_block(int bid, int BH, int T, bool heavy_hig
     *tile = heavy_high ? (T - 1 - rank) : rank;
 }
 
-// Rows of one attention problem (a query head of one sequence) and the number
-// of its tokens.  Dense batches ([B, H, N, d], cu == nullptr): query head
-// bh = b * Hq + h starts at row bh * N of Q and reads key/value head bh / G.
-// Packed sequences ([H, total, d]): bh = s * Hq + h is head h over tokens
-// [cu[s], cu[s + 1]); the offsets are clamped to [0, total] and the length to
-// Nmax, so malformed offsets cannot address rows outside the tensors.
+// Rows of one attention problem (a query head of one sequence) and its query
+// and key counts.  Dense batches ([B, H, N, d], cu == nullptr): query head
+// bh = b * Hq + h starts at row bh * N of Q and reads key/value head bh / G;
+// nq = nk = N.  Packed sequences (query-side tensors [H, total, d], key-side
+// [H, total_k, d]): bh = s * Hq + h is head h over queries [cu[s], cu[s + 1])
+// and keys [cu_k[s], cu_k[s + 1]); the offsets are clamped to the tensors and
+// the counts to the longest runs, so malformed offsets cannot address rows
+// outside the tensors.  With causal masking query i sees key j iff
+// j <= i + (nk - nq): the diagonal is aligned at the last query and key.
 struct SeqRows {
-    size_t q0;   // first row of the query-head tensors (Q, O, dO, dQ; LSE and row statistics)
+    size_t q0;   // first row of the query-head tensors (Q, O, dO, dQ; LSE, row statistics)
     size_t kv0;  // first row of the key/value-head tensors (K, V, dK, dV)
-    int n;       // tokens of this problem
+    size_t p0;   // first row of this query head's key-side FP32 partials (grouped heads)
+    int nq;      // queries of this problem
+    int nk;      // keys of this problem
 };
-__device__ __forceinline__ SeqRows seq_rows(const int* cu, int bh, int Nmax, int G, int Hq,
-                                            int total) {
-    if (cu == nullptr) return {(size_t)bh * Nmax, (size_t)(bh / G) * Nmax, Nmax};
+__device__ __forceinline__ SeqRows seq_rows(const int* cu, const int* cu_k, int bh, int Nq_max,
+                                            int Nk_max, int G, int Hq, int total, int total_k) {
+    if (cu == nullptr)
+        return {(size_t)bh * Nq_max, (size_t)(bh / G) * Nq_max, (size_t)bh * Nq_max, Nq_max,
+                Nq_max};
     const int s = bh / Hq, h = bh - s * Hq;
     const int a = min(max(cu[s], 0), total);
     const int b = min(max(cu[s + 1], a), total);
-    return {(size_t)h * total + a, (size_t)(h / G) * total + a, min(b - a, Nmax)};
+    const int ak = min(max(cu_k[s], 0), total_k);
+    const int bk = min(max(cu_k[s + 1], ak), total_k);
+    return {(size_t)h * total + a, (size_t)(h / G) * total_k + ak, (size_t)h * total_k + ak,
+            min(b - a, Nq_max), min(bk - ak, Nk_max)};
+}
+
+// Floor division by a positive divisor, also for negative numerators.
+__device__ __forceinline__ int floor_div(int a, int b) { return a >= 0 ? a / b : -((-a + b - 1) / b); }
+
+// Key tiles of a 64-query tile: keys [0, 64 * nkv) hold every key a query of
+// the tile can see, and tiles [nplain, nkv) need masks (at most two: the
+// causal diagonal crosses at most two key tiles, and the key tail).
+struct KeyRange {
+    int nkv, nplain;
+};
+__device__ __forceinline__ KeyRange key_range(int qtile, int Nk, int off, int causal) {
+    const int kv_end = causal ? min(max((qtile + 1) * kTile + off, 0), Nk) : Nk;
+    const int nkv = (kv_end + kTile - 1) / kTile;
+    // fully visible tiles: every key <= the first query's last visible key, and
+    // no key beyond Nk
+    const int nfull = causal ? floor_div(qtile * kTile + off + 1, kTile) : Nk / kTile;
+    return {nkv, max(0, min(min(nfull, Nk / kTile), nkv))};
 }
 
 // Target waves per SIMD of each MFMA kernel (build-time tuning constants).

@@ -45,7 +45,7 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, uint16_t* __restrict__ O, float* __restrict__ LSE,
     int BH, int Nmax, int causal, float scale, int G, const int* __restrict__ cu, int Hq,
-    int total) {
+    int total, const int* __restrict__ cu_k, int total_k, int Nkmax) {
     constexpr int MB = D / 16;
     constexpr int KC = D / 32;
     constexpr int PER_NB = MB * 4 + 2;  // acc, m, l of one query block
@@ -57,9 +57,10 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
     const int T = (Nmax + kTile - 1) / kTile;  // tiles of the longest problem
     int bh, tile;
     map_block(blockIdx.x, BH, T, causal != 0, &bh, &tile);
-    const SeqRows sr = seq_rows(cu, bh, Nmax, G, Hq, total);
-    const int N = sr.n;
+    const SeqRows sr = seq_rows(cu, cu_k, bh, Nmax, Nkmax, G, Hq, total, total_k);
+    const int N = sr.nq, Nk = sr.nk;
     if (tile * kTile >= N) return;  // a shorter sequence has no such tile
+    const int off = Nk - N;           // causal: query i sees key j iff j <= i + off
     const size_t hoff = sr.q0 * D;    // query head: Q, O
     const size_t kvoff = sr.kv0 * D;  // its key/value head
     const int tid = threadIdx.x;
@@ -88,13 +89,12 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int kv_end = causal ? min(N, (tile + 1) * kTile) : N;
-    const int nkv = (kv_end + kTile - 1) / kTile;
-    // Only the last key tile can need masks: the diagonal tile (causal) or the
-    // key tail (N not a multiple of the tile).
-    const int nplain = (causal || (N % kTile)) ? nkv - 1 : nkv;
+    // Only the last one or two key tiles need masks (the causal diagonal, the
+    // key tail).
+    const KeyRange kr = key_range(tile, Nk, off, causal);
+    const int nkv = kr.nkv, nplain = kr.nplain;
 
-    // Rows beyond N are never written by the DMA: zero both buffers once so
+    // Rows beyond Nk are never written by the DMA: zero both buffers once so
     // every value a product can read is finite.
     {
         u32x4* z0 = reinterpret_cast<u32x4*>(&KV0[0][0]);
@@ -110,8 +110,8 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
 
     TileDma<D> dma;
     dma.init(lane, wave);
-    dma.load(K + kvoff, KV0[0], 0, N);
-    dma.load(V + kvoff, KV0[1], 0, N);
+    dma.load(K + kvoff, KV0[0], 0, Nk);
+    dma.load(V + kvoff, KV0[1], 0, Nk);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
@@ -120,8 +120,8 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
         constexpr bool MASK = decltype(masked)::value;
         const int k0 = kt * kTile;
         if (kt + 1 < nkv) {
-            dma.load(K + kvoff, Kn, k0 + kTile, N);
-            dma.load(V + kvoff, Vn, k0 + kTile, N);
+            dma.load(K + kvoff, Kn, k0 + kTile, Nk);
+            dma.load(V + kvoff, Vn, k0 + kTile, Nk);
         }
         // Keep the loads of the next tile at the top of the step: left alone,
         // the scheduler sinks them next to the closing wait, which exposes
@@ -150,7 +150,7 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
                     for (int i = 0; i < 4; ++i) {
                         const int key = k0 + 32 * kh + kb * 16 + 4 * g + i;
                         const int qrow = q0w + nb * 16 + c16;
-                        const bool ok = key < N && (!causal || key <= qrow);
+                        const bool ok = key < Nk && (!causal || key <= qrow + off);
                         s[nb][kb][i] = ok ? s[nb][kb][i] : -INFINITY;
                     }
         }
@@ -205,9 +205,14 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
     }
     if (kt < nplain) {
         step(plain, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
-        if (kt + 1 < nkv) step(masked, kt + 1, KV1[0], KV1[1], KV0[0], KV0[1]);
-    } else if (kt < nkv) {
-        step(masked, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
+        ++kt;
+    }
+    // Tile kt lives in buffer kt mod 2.
+    for (; kt < nkv; ++kt) {
+        if (kt & 1)
+            step(masked, kt, KV1[0], KV1[1], KV0[0], KV0[1]);
+        else
+            step(masked, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
     }
 
     // Merge the two key halves of each query (waves w and w + 2): waves 2, 3
@@ -244,19 +249,22 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
         const float ltot = xor_sum(lrun[nb] * fa + lo * fb);
         const int qrow = q0w + nb * 16 + c16;
         if (qrow < N) {
+            // A query that sees no key (l = 0; a visible key adds z = 1) gets
+            // O = 0 and LSE = +inf, so the backward's P is 0 on its row.
+            const bool empty = !(ltot > 0.f);
             uint16_t* orow = O + hoff + (size_t)qrow * D;
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb) {
                 float v[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    v[i] = (acc[nb][mb][i] * fa + p[(mb * 4 + i) * 64] * fb) / ltot;
+                    v[i] = empty ? 0.f : (acc[nb][mb][i] * fa + p[(mb * 4 + i) * 64] * fb) / ltot;
                 st_bf16x4(orow + mb * 16 + 4 * g, v[0], v[1], v[2], v[3]);
             }
             if (g == 0) {
 #pragma clang fp contract(off)
                 const float lse = scale * mt + logf(ltot);
-                LSE[sr.q0 + qrow] = lse;
+                LSE[sr.q0 + qrow] = empty ? INFINITY : lse;
             }
         }
     }
@@ -274,7 +282,7 @@ __global__ __launch_bounds__(kThreads, GPA_FWD16_OCC) void fwd_sbs_q16_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, uint16_t* __restrict__ O, float* __restrict__ LSE,
     int BH, int Nmax, int causal, float scale, int G, const int* __restrict__ cu, int Hq,
-    int total) {
+    int total, const int* __restrict__ cu_k, int total_k, int Nkmax) {
     constexpr int MB = D / 16;
     constexpr int KC = D / 32;
     __shared__ __attribute__((aligned(16))) uint16_t KV0[2][kTile * D];
@@ -283,9 +291,10 @@ __global__ __launch_bounds__(kThreads, GPA_FWD16_OCC) void fwd_sbs_q16_kernel(
     const int T = (Nmax + kTile - 1) / kTile;  // tiles of the longest problem
     int bh, tile;
     map_block(blockIdx.x, BH, T, causal != 0, &bh, &tile);
-    const SeqRows sr = seq_rows(cu, bh, Nmax, G, Hq, total);
-    const int N = sr.n;
+    const SeqRows sr = seq_rows(cu, cu_k, bh, Nmax, Nkmax, G, Hq, total, total_k);
+    const int N = sr.nq, Nk = sr.nk;
     if (tile * kTile >= N) return;  // a shorter sequence has no such tile
+    const int off = Nk - N;  // causal: query i sees key j iff j <= i + off
     const size_t hoff = sr.q0 * D;
     const size_t kvoff = sr.kv0 * D;
     const int tid = threadIdx.x;
@@ -306,15 +315,14 @@ __global__ __launch_bounds__(kThreads, GPA_FWD16_OCC) void fwd_sbs_q16_kernel(
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int kv_end = causal ? min(N, (tile + 1) * kTile) : N;
-    const int nkv = (kv_end + kTile - 1) / kTile;
-    const int nplain = (causal || (N % kTile)) ? nkv - 1 : nkv;
+    const KeyRange kr = key_range(tile, Nk, off, causal);
+    const int nkv = kr.nkv, nplain = kr.nplain;
 
     TileDma<D> dma;
     dma.init(lane, wave);
     wait_vm_lgkm0<0>();
-    dma.load(K + kvoff, KV0[0], 0, N);
-    dma.load(V + kvoff, KV0[1], 0, N);
+    dma.load(K + kvoff, KV0[0], 0, Nk);
+    dma.load(V + kvoff, KV0[1], 0, Nk);
     wait_vm_lgkm0<0>();
     __builtin_amdgcn_s_barrier();
 
@@ -323,8 +331,8 @@ __global__ __launch_bounds__(kThreads, GPA_FWD16_OCC) void fwd_sbs_q16_kernel(
         constexpr bool MASK = decltype(masked)::value;
         const int k0 = kt * kTile;
         if (kt + 1 < nkv) {
-            dma.load(K + kvoff, Kn, k0 + kTile, N);
-            dma.load(V + kvoff, Vn, k0 + kTile, N);
+            dma.load(K + kvoff, Kn, k0 + kTile, Nk);
+            dma.load(V + kvoff, Vn, k0 + kTile, Nk);
         }
         __builtin_amdgcn_sched_barrier(0);
         // S^T[key][query]: s[kb] holds keys 16 kb + 4g + i for this lane's query.
@@ -343,7 +351,7 @@ __global__ __launch_bounds__(kThreads, GPA_FWD16_OCC) void fwd_sbs_q16_kernel(
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int key = k0 + kb * 16 + 4 * g + i;
-                    const bool ok = key < N && (!causal || key <= qrow);
+                    const bool ok = key < Nk && (!causal || key <= qrow + off);
                     s[kb][i] = ok ? s[kb][i] : -INFINITY;
                 }
         }
@@ -393,25 +401,33 @@ __global__ __launch_bounds__(kThreads, GPA_FWD16_OCC) void fwd_sbs_q16_kernel(
     }
     if (kt < nplain) {
         step(plain, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
-        if (kt + 1 < nkv) step(masked, kt + 1, KV1[0], KV1[1], KV0[0], KV0[1]);
-    } else if (kt < nkv) {
-        step(masked, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
+        ++kt;
+    }
+    // Tile kt lives in buffer kt mod 2.
+    for (; kt < nkv; ++kt) {
+        if (kt & 1)
+            step(masked, kt, KV1[0], KV1[1], KV0[0], KV0[1]);
+        else
+            step(masked, kt, KV0[0], KV0[1], KV1[0], KV1[1]);
     }
 
     const float ltot = xor_sum(lrun);
     if (qrow < N) {
+        // A query that sees no key (l = 0; a visible key adds z = 1) gets O = 0
+        // and LSE = +inf, so the backward's P is 0 on its row.
+        const bool empty = !(ltot > 0.f);
         uint16_t* orow = O + hoff + (size_t)qrow * D;
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
             float v[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) v[i] = acc[mb][i] / ltot;
+            for (int i = 0; i < 4; ++i) v[i] = empty ? 0.f : acc[mb][i] / ltot;
             st_bf16x4(orow + mb * 16 + 4 * g, v[0], v[1], v[2], v[3]);
         }
         if (g == 0) {
 #pragma clang fp contract(off)
             const float lse = scale * mrun + logf(ltot);
-            LSE[sr.q0 + qrow] = lse;
+            LSE[sr.q0 + qrow] = empty ? INFINITY : lse;
         }
     }
 }
@@ -426,7 +442,8 @@ hipError_t launch_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, u
     // blocks per wave, whose halved LDS reads matter more there.
 #define GPA_FWD(KERNEL, DD, FM)                                                               \
     KERNEL<DD, FM><<<grid, block, 0, st>>>(Q, K, V, O, LSE, s.BH, s.N, s.causal, s.scale, s.G, \
-                                           s.cu, s.Hq, s.total)
+                                           s.cu, s.Hq, s.total, s.cu_k, s.total_k,             \
+                                           s.Nk > 0 ? s.Nk : s.N)
     if (s.d == 64) {
         if (fma_forward) GPA_FWD(fwd_sbs_q16_kernel, 64, true);
         else GPA_FWD(fwd_sbs_q16_kernel, 64, false);

@@ -16,11 +16,16 @@ struct Shape {
     int G;         // query heads per key/value head (1: multi-head attention);
                    // query head bh reads key/value head bh / G
     // Packed variable-length sequences (nullptr: dense [B, H, N, d] batches).
-    // Tensors are [H, total, d]; sequence s holds tokens [cu[s], cu[s + 1]) and
-    // problem bh = s * Hq + h is head h of sequence s.
-    const int* cu = nullptr;  // device, nseq + 1 offsets
-    int Hq = 1;               // query heads
-    int total = 0;            // tokens in the packed tensors
+    // Query-side tensors are [H, total, d] and key-side ones [H, total_k, d];
+    // sequence s holds queries [cu[s], cu[s + 1]) and keys
+    // [cu_k[s], cu_k[s + 1]), and problem bh = s * Hq + h is head h of
+    // sequence s.  N is then the longest query run and Nk the longest key run.
+    const int* cu = nullptr;    // device, nseq + 1 query offsets
+    int Hq = 1;                 // query heads
+    int total = 0;              // query tokens in the packed tensors
+    const int* cu_k = nullptr;  // device, nseq + 1 key offsets
+    int total_k = 0;            // key tokens in the packed tensors
+    int Nk = 0;                 // longest key run (dense: N)
 };
 
 // Kernel ids for timing (gpa_profile_*).

@@ -14,8 +14,11 @@ stores BF16 bit patterns: it holds none of the attention arithmetic.
 
 A case is either dense ([B, H, N, d] tensors) or packed ([H, total, d]
 tensors with sequence offsets cu, sequence s = tokens cu[s] .. cu[s+1]-1).
+A packed case may give its keys their own lengths (lens_k, offsets cu_k, key
+axis of total_k tokens); otherwise the keys share the query lengths.
 Every query head h draws, from Generator(PCG64(SeedSequence([seed, index,
-h]))), standard normal (total, d) arrays Q0, K0, V0, U0 in that order, then
+h]))), standard normal arrays Q0 (total, d), K0, V0 (total_k, d) and
+U0 (total, d) in that order, then
 the per-channel biases kb ~ N(0, k_shift^2), vb ~ N(0, v_shift^2) and
 qb ~ N(0, q_bias^2) (zero when the spread is 0), then for constant values one
 row c ~ N(0, 1):
@@ -53,18 +56,51 @@ class SuiteCase:
     v_shift: float = 0.0
     v_const: bool = False
     do_std: float = 1.0
+    lens_k: tuple = ()     # packed only: key lengths when they differ from lens
+
+    @property
+    def cross(self) -> bool:
+        """Keys have lengths of their own."""
+        return len(self.lens_k) > 0
+
+    @property
+    def key_lens(self) -> tuple:
+        return self.lens_k if self.cross else self.lens
 
     @property
     def total(self) -> int:
         return int(sum(self.lens))
 
     @property
+    def total_k(self) -> int:
+        return int(sum(self.key_lens))
+
+    @property
     def cu(self) -> np.ndarray:
         return np.concatenate([[0], np.cumsum(self.lens)]).astype(np.int32)
 
     @property
+    def cu_k(self) -> np.ndarray:
+        return np.concatenate([[0], np.cumsum(self.key_lens)]).astype(np.int32)
+
+    @property
     def max_seqlen(self) -> int:
         return int(max(self.lens))
+
+    @property
+    def max_seqlen_k(self) -> int:
+        return int(max(self.key_lens))
+
+    def empty_rows(self) -> np.ndarray:
+        """Boolean [total]: queries that see no key (no keys in their
+        sequence, or, with causal, the first nq - nk queries)."""
+        e = np.zeros(self.total, dtype=bool)
+        for a, nq, nk in zip(self.cu[:-1], self.lens, self.key_lens):
+            if nk == 0:
+                e[a:a + nq] = True
+            elif self.causal and nq > nk:
+                e[a:a + nq - nk] = True
+        return e
 
     @property
     def scale(self) -> float:
@@ -134,6 +170,24 @@ def _cases():
     add("d128 key shift", "head dim 128", (300,), packed=False, d=128, k_shift=64.0)
     add("d128 constant values", "head dim 128", (80,), packed=False, d=128, v_const=True)
     add("d128 sharp", "head dim 128", (256,), packed=False, d=128, q_std=20.0)
+    # Queries and keys of unequal lengths in one sequence (the causal diagonal
+    # aligned at the last query and key): fewer queries than keys, more
+    # queries than keys (leading queries see no key), sequences without keys.
+    add("fewer queries than keys", "unequal query/key", (30, 100, 64), lens_k=(100, 130, 64))
+    add("fewer queries, tile-aligned offset", "unequal query/key", (64, 100),
+        lens_k=(192, 228))
+    add("more queries than keys", "unequal query/key", (100, 70, 130), lens_k=(40, 70, 2))
+    add("sequences without keys", "unequal query/key", (20, 50, 5), lens_k=(0, 80, 0))
+    add("single queries on long keys", "unequal query/key", (1, 1, 1, 1),
+        lens_k=(500, 64, 1, 129))
+    add("non-causal unequal query/key", "unequal query/key", (50, 200, 3), causal=False,
+        lens_k=(300, 17, 64))
+    add("whole query tiles without keys", "unequal query/key", (200,), lens_k=(10,))
+    add("d128 unequal query/key", "unequal query/key", (100, 33), d=128, lens_k=(37, 200))
+    add("d128 fewer queries, tile-aligned offset", "unequal query/key", (64, 40), d=128,
+        lens_k=(128, 104))
+    add("non-causal sequence without keys", "unequal query/key", (10, 20), causal=False,
+        lens_k=(30, 0))
     return C
 
 
@@ -141,22 +195,23 @@ CASES = _cases()
 
 
 def make_case(case: SuiteCase, seed: int = 7000):
-    """BF16 bit arrays of one case: q, do [Hq, total, d] and k, v [Hkv, total,
-    d] on the packed axis (dense cases: B consecutive blocks of N tokens)."""
-    T, d, Hq, Hkv = case.total, case.d, case.Hq, case.Hkv
+    """BF16 bit arrays of one case: q, do [Hq, total, d] and k, v [Hkv,
+    total_k, d] on the packed axis (dense cases: B consecutive blocks of N
+    tokens)."""
+    T, Tk, d, Hq, Hkv = case.total, case.total_k, case.d, case.Hq, case.Hkv
     G = Hq // Hkv
     out = {"q": np.empty((Hq, T, d), np.uint16), "do": np.empty((Hq, T, d), np.uint16),
-           "k": np.empty((Hkv, T, d), np.uint16), "v": np.empty((Hkv, T, d), np.uint16)}
+           "k": np.empty((Hkv, Tk, d), np.uint16), "v": np.empty((Hkv, Tk, d), np.uint16)}
     for h in range(Hq):
         rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, case.index, h])))
-        q0, k0, v0, u0 = (rng.standard_normal((T, d)) for _ in range(4))
+        q0, k0, v0, u0 = (rng.standard_normal((n, d)) for n in (T, Tk, Tk, T))
         kb = rng.normal(0.0, case.k_shift, d) if case.k_shift > 0 else np.zeros(d)
         vb = rng.normal(0.0, case.v_shift, d) if case.v_shift > 0 else np.zeros(d)
         qb = rng.normal(0.0, case.q_bias, d) if case.q_bias > 0 else np.zeros(d)
         crow = rng.standard_normal(d)
         q = case.q_std * q0 + qb[None, :]
         k = k0 + kb[None, :]
-        v = np.broadcast_to(crow, (T, d)) if case.v_const else v0 + vb[None, :]
+        v = np.broadcast_to(crow, (Tk, d)) if case.v_const else v0 + vb[None, :]
         u = case.do_std * u0 if case.do_std > 0 else np.zeros((T, d))
         out["q"][h] = f32_to_bf16_bits(q.astype(np.float32))
         out["do"][h] = f32_to_bf16_bits(u.astype(np.float32))

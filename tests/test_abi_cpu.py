@@ -123,31 +123,45 @@ def test_gqa_validation(lib):
     assert gqa == mha + 2 * 16 * 4096 * 64 * 4
 
 
-def _fwd_varlen(lib, cu=FAKE + 0x50000000, nseq=3, total=300, Hq=4, Hkv=2, ms=128, d=64,
-                O=FAKE + 0x30000000):
+def _fwd_varlen(lib, cu=FAKE + 0x50000000, cu_k=None, nseq=3, total=300, total_k=300, Hq=4,
+                Hkv=2, ms=128, ms_k=128, d=64, O=FAKE + 0x30000000):
     P = FAKE
     return lib.gpa_attn_fwd_varlen(P, P + 0x10000000, P + 0x20000000, O, P + 0x40000000, cu,
-                                   nseq, total, Hq, Hkv, ms, d, 1, 0.125, None)
+                                   cu_k, nseq, total, total_k, Hq, Hkv, ms, ms_k, d, 1, 0.125, None)
 
 
 def test_varlen_validation(lib):
     assert _fwd_varlen(lib, cu=None) == 1
-    assert b"cu_seqlens is NULL" in lib.gpa_last_error()
+    assert b"cu_seqlens_q is NULL" in lib.gpa_last_error()
     assert _fwd_varlen(lib, cu=FAKE + 0x50000002) == 1                 # not 4-byte aligned
+    assert _fwd_varlen(lib, cu_k=FAKE + 0x60000002) == 1
     assert _fwd_varlen(lib, ms=301) == 1                               # longer than total
     assert _fwd_varlen(lib, ms=0) == 1
     assert _fwd_varlen(lib, nseq=0) == 1
     assert _fwd_varlen(lib, Hq=6, Hkv=4) == 1
     assert _fwd_varlen(lib, d=96) == 2
-    assert _fwd_varlen(lib, O=FAKE + 0x50000000) == 1                  # O overlaps cu_seqlens
+    assert _fwd_varlen(lib, O=FAKE + 0x50000000) == 1                  # O overlaps cu_seqlens_q
     assert b"overlaps" in lib.gpa_last_error()
-    # workspace: row statistics over [Hq, total], tile blocks per (sequence, head)
-    ws = lib.gpa_attn_bwd_varlen_workspace_bytes(3, 300, 4, 2, 128, 64, 2)
+    # the key side: its own total and longest run, checked on their own
+    assert _fwd_varlen(lib, cu_k=FAKE + 0x60000000, total_k=200, ms_k=201) == 1
+    assert _fwd_varlen(lib, cu_k=FAKE + 0x60000000, total_k=0, ms_k=0) == 1
+    assert _fwd_varlen(lib, cu_k=FAKE + 0x60000000, O=FAKE + 0x60000000) == 1
+    assert b"cu_seqlens_k" in lib.gpa_last_error()
+    # shared offsets (cu_seqlens_k NULL) need matching totals and runs
+    assert _fwd_varlen(lib, total_k=200) == 1
+    assert _fwd_varlen(lib, ms_k=64) == 1
+    assert b"shared offsets" in lib.gpa_last_error()
+    # workspace: row statistics over [Hq, total_q], tile blocks per (sequence,
+    # head) and 64 query rows, z over the queries, grouped partials over the keys
+    ws = lib.gpa_attn_bwd_varlen_workspace_bytes(3, 300, 300, 4, 2, 128, 128, 64, 2)
     assert ws >= 4 * 4 * 300 * 4 + 3 * 4 * 2 * 512 + 4 * 300 * 64 * 2 + 2 * 4 * 300 * 64 * 4
-    assert lib.gpa_attn_bwd_varlen_workspace_bytes(3, 300, 4, 2, 301, 64, 2) == 0
-    assert lib.gpa_attn_bwd_varlen_workspace_bytes(3, 300, 4, 2, 128, 64, 3) == 0
+    ws_k = lib.gpa_attn_bwd_varlen_workspace_bytes(3, 300, 500, 4, 2, 128, 256, 64, 2)
+    assert ws_k - ws == 2 * 4 * 200 * 64 * 4
+    assert lib.gpa_attn_bwd_varlen_workspace_bytes(3, 300, 300, 4, 2, 301, 128, 64, 2) == 0
+    assert lib.gpa_attn_bwd_varlen_workspace_bytes(3, 300, 300, 4, 2, 128, 301, 64, 2) == 0
+    assert lib.gpa_attn_bwd_varlen_workspace_bytes(3, 300, 300, 4, 2, 128, 128, 64, 3) == 0
     # the backward rejects a short workspace before launching anything
     P = FAKE
     args = [P + i * 0x10000000 for i in range(9)]
-    assert lib.gpa_attn_bwd_varlen(*args, P + 0x90000000, 3, 300, 4, 2, 128, 64, 1, 0.125, 2,
-                                   P + 0xA0000000, 16, None) == 3
+    assert lib.gpa_attn_bwd_varlen(*args, P + 0x90000000, None, 3, 300, 300, 4, 2, 128, 128, 64,
+                                   1, 0.125, 2, P + 0xA0000000, 16, None) == 3

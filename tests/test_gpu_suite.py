@@ -12,6 +12,9 @@ reported, not gated (the paper's FA3-SBS fails its shifted cases).
 
 Packed runs must also equal dense runs of each sequence alone bit for bit:
 a sequence of a pack is the same attention problem, solved by the same kernels.
+Sequences whose queries and keys differ in number are checked the same way
+against the square problem they reduce to (queries padded at the top with
+zero rows, or cut to the last nk queries when the leading ones see no key).
 """
 import numpy as np
 import pytest
@@ -52,6 +55,14 @@ def _packed(t, B):
     return a.transpose(1, 0, 2).reshape(a.shape[1], -1)
 
 
+def key_offsets(case):
+    """Keyword arguments for the key side of a packed case."""
+    if not case.cross:
+        return {}
+    return dict(cu_seqlens_k=torch.tensor(case.cu_k, dtype=torch.int32, device="cuda:0"),
+                max_seqlen_k=case.max_seqlen_k)
+
+
 def run_case(gpa, case, x):
     """Forward and the three backward modes; host float64 results on the
     packed axis, plus BF16 bit patterns for the identity checks."""
@@ -59,9 +70,10 @@ def run_case(gpa, case, x):
     if case.packed:
         q, k, v, u = (G.to_dev(x[n]) for n in ("q", "k", "v", "do"))
         cu = torch.tensor(case.cu, dtype=torch.int32, device="cuda:0")
-        o, lse = gpa.attn_fwd_varlen(q, k, v, cu, case.max_seqlen, case.causal, case.scale)
+        kw = key_offsets(case)
+        o, lse = gpa.attn_fwd_varlen(q, k, v, cu, case.max_seqlen, case.causal, case.scale, **kw)
         res = {m: gpa.attn_bwd_varlen(q, k, v, o, lse, u, cu, case.max_seqlen, m, case.causal,
-                                      case.scale, return_stats=True) for m in MODES}
+                                      case.scale, return_stats=True, **kw) for m in MODES}
         torch.cuda.synchronize()
         host = G.to_host
     else:
@@ -76,6 +88,7 @@ def run_case(gpa, case, x):
     out["O_bits"] = G.bits(o)
     for m, (dq, dk, dv, st) in res.items():
         out[m] = dict(dQ=host(dq), dK=host(dk), dV=host(dv), m=host(st["m"]),
+                      lam=host(st["lambda"]), rho=host(st["rho"]),
                       bits={n: G.bits(t) for n, t in (("dQ", dq), ("dK", dk), ("dV", dv))})
     return out
 
@@ -96,7 +109,8 @@ def test_suite_case(gpa, case):
     G.log(f"suite case {case.index:03d} {case.name}: lens={case.lens[:6]}{'...' if len(case.lens) > 6 else ''} "
           f"packed={case.packed} causal={case.causal} Hq={case.Hq} Hkv={case.Hkv} d={case.d}")
     x = suite.make_case(case)
-    ex = oracle.exact_varlen(x["q"], x["k"], x["v"], x["do"], case.cu, case.causal, case.scale)
+    ex = oracle.exact_varlen(x["q"], x["k"], x["v"], x["do"], case.cu, case.causal, case.scale,
+                             cu_seqlens_k=case.cu_k)
     out = run_case(gpa, case, x)
     report = {}
     for m in ("plain", "gproj"):
@@ -119,9 +133,19 @@ def test_suite_case(gpa, case):
         assert gk[0] <= 1.05 * pk[0] + 1e-3, (pk, gk)
     else:
         assert gk[1] <= max(1.05 * pk[1], ZERO_ABS), (pk, gk)
-    # operand mass of every row (every row here sees at least its own key)
-    mass = out["gproj"]["m"]
+    # operand mass of every row that sees a key; a row that sees none is
+    # empty: O = 0, LSE = +inf, and m = rho = lambda = 0, dQ = 0 in every mode
+    empty = case.empty_rows()
+    mass = out["gproj"]["m"][:, ~empty]
     assert np.all((mass > 0.99) & (mass < 1.01)), (mass.min(), mass.max())
+    if empty.any():
+        assert np.all(out["O"][:, empty] == 0.0)
+        assert np.all(np.isposinf(out["LSE"][:, empty]))
+        for m in MODES:
+            assert np.all(out[m]["dQ"][:, empty] == 0.0), m
+        for n in ("m", "rho", "lam"):
+            assert np.all(out["gproj"][n][:, empty] == 0.0), n
+    assert np.all(np.isfinite(out["LSE"][:, ~empty]))
     if case.name == "singleton":
         assert np.all(out["gproj"]["dQ"] == 0.0)
         assert np.abs(out["gproj"]["dK"]).max() <= ZERO_ABS
@@ -158,6 +182,62 @@ def test_packed_equals_dense_per_sequence(gpa, idx):
                 assert np.array_equal(G.bits(a)[0], G.bits(p)[:, lo:hi]), (m, name, lo, hi)
 
 
+CROSS = [c.index for c in suite.CASES if c.cross and c.causal]
+
+
+@pytest.mark.parametrize("idx", CROSS)
+def test_unequal_query_key_equals_square(gpa, idx):
+    """A causal sequence with nq queries and nk keys is the square problem on
+    its keys with the queries aligned at the end: nq < nk pads the queries at
+    the top with nk - nq zero rows of zero upstream gradient, nq > nk keeps
+    the last nk queries (the others see no key).  Per-row results (O, LSE,
+    dQ) match the square run bit for bit; dK and dV do too when nk - nq is a
+    multiple of the 64-row tile (the padding rows add exact zeros, and the
+    query tiles then line up)."""
+    case = suite.CASES[idx]
+    x = suite.make_case(case)
+    G.log(f"unequal query/key vs square: case {idx:03d} {case.name}")
+    q, k, v, u = (G.to_dev(x[n]) for n in ("q", "k", "v", "do"))
+    cu = torch.tensor(case.cu, dtype=torch.int32, device="cuda:0")
+    kw = key_offsets(case)
+    o, lse = gpa.attn_fwd_varlen(q, k, v, cu, case.max_seqlen, True, case.scale, **kw)
+    pk = {m: gpa.attn_bwd_varlen(q, k, v, o, lse, u, cu, case.max_seqlen, m, True, case.scale,
+                                 **kw) for m in MODES}
+    torch.cuda.synchronize()
+    ob, lh = G.bits(o), lse.cpu().numpy()
+    pb = {m: [G.bits(t) for t in pk[m]] for m in MODES}
+    Hq, d = case.Hq, case.d
+    for s in range(len(case.lens)):
+        a, b = int(case.cu[s]), int(case.cu[s + 1])
+        ka, kb = int(case.cu_k[s]), int(case.cu_k[s + 1])
+        nq, nk = b - a, kb - ka
+        if nq == 0 or nk == 0:
+            continue
+        if nq <= nk:
+            pad, first = nk - nq, a
+            z = np.zeros((Hq, pad, d), np.uint16)
+            qs = np.concatenate([z, x["q"][:, a:b]], 1)
+            us = np.concatenate([z, x["do"][:, a:b]], 1)
+            rows = slice(pad, nk)
+        else:
+            first = a + nq - nk
+            qs, us = x["q"][:, first:b], x["do"][:, first:b]
+            rows = slice(0, nk)
+        qd, ud = G.to_dev(qs[None]), G.to_dev(us[None])
+        kd, vd = G.to_dev(x["k"][None, :, ka:kb]), G.to_dev(x["v"][None, :, ka:kb])
+        od, lsed = gpa.attn_fwd(qd, kd, vd, True, case.scale)
+        assert np.array_equal(G.bits(od)[0][:, rows], ob[:, first:b]), s
+        assert np.array_equal(lsed[0].cpu().numpy()[:, rows], lh[:, first:b]), s
+        aligned = (nk - nq) % 64 == 0
+        for m in MODES:
+            dq, dk, dv = (G.bits(t)[0] for t in gpa.attn_bwd(qd, kd, vd, od, lsed, ud, m, True,
+                                                             case.scale))
+            assert np.array_equal(dq[:, rows], pb[m][0][:, first:b]), (m, s)
+            if aligned:
+                assert np.array_equal(dk, pb[m][1][:, ka:kb]), (m, s)
+                assert np.array_equal(dv, pb[m][2][:, ka:kb]), (m, s)
+
+
 def test_packed_reproducible(gpa):
     """Repeated runs of a packed case are bitwise identical."""
     case = suite.CASES[46]
@@ -187,3 +267,9 @@ def test_varlen_rejects_bad_arguments(gpa):
         gpa.attn_fwd_varlen(q, k, v, cu, 0, True, case.scale)
     with pytest.raises(ValueError):
         gpa.attn_fwd_varlen(q, k, v, cu.to(torch.int64), case.max_seqlen, True, case.scale)
+    with pytest.raises(ValueError):  # keys of their own length need their own offsets
+        gpa.attn_fwd_varlen(q, k[:, :-1].contiguous(), v[:, :-1].contiguous(), cu,
+                            case.max_seqlen, True, case.scale)
+    with pytest.raises(gpa.GpaError):  # the key side's longest run exceeds its total
+        gpa.attn_fwd_varlen(q, k, v, cu, case.max_seqlen, True, case.scale, cu_seqlens_k=cu,
+                            max_seqlen_k=case.total + 1)

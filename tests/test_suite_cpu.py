@@ -37,3 +37,27 @@ def test_draws_reproducible_and_recipes_hold(idx):
         assert np.all(bf16_bits_to_f32(a["do"]) == 0)
     other = suite.make_case(c, seed=7001)
     assert not np.array_equal(other["q"], a["q"])
+
+
+def test_unequal_query_key_cases():
+    cross = [c for c in suite.CASES if c.cross]
+    assert len(cross) >= 8
+    for c in cross:
+        assert c.packed and len(c.lens_k) == len(c.lens)
+        assert c.cu_k[0] == 0 and c.cu_k[-1] == c.total_k >= 1 and np.all(np.diff(c.cu_k) >= 0)
+        assert c.max_seqlen_k == max(c.lens_k) >= 1
+        x = suite.make_case(c)
+        assert x["q"].shape == (c.Hq, c.total, c.d) and x["do"].shape == x["q"].shape
+        assert x["k"].shape == (c.Hkv, c.total_k, c.d) and x["v"].shape == x["k"].shape
+    # leading queries of a causal sequence with nq > nk see no key, and so
+    # does every query of a sequence without keys
+    more = next(c for c in cross if c.name == "more queries than keys")
+    e = more.empty_rows()
+    assert e.sum() == (100 - 40) + 0 + (130 - 2)
+    assert e[:60].all() and not e[60:100].any() and e[170:298].all() and not e[298:].any()
+    none = next(c for c in cross if c.name == "sequences without keys")
+    assert none.empty_rows().sum() == 20 + 5
+    nc = next(c for c in cross if c.name == "non-causal sequence without keys")
+    assert nc.empty_rows().tolist() == [False] * 10 + [True] * 20
+    # square cases have no empty rows unless a sequence is empty
+    assert not any(c.empty_rows().any() for c in suite.CASES if not c.cross)
