@@ -293,14 +293,29 @@ __device__ __forceinline__ float xor_sum(float v) {
 // schedule for any number of resident workgroups.  heavy_high selects which
 // end is heavy: the query-major causal kernels' last tiles do the most work,
 // the key-major kernels' first tiles do.
+//
+// snake_rounds: an XCD places its i-th workgroup on compute unit i mod 32
+// while it has free slots, so the first `resident` x 32 workgroups of an XCD
+// (resident = workgroups a unit holds) are placed before any finishes.
+// Reversing every other block of 32 of those positions deals the heavy-first
+// list out like a snake draft: compute unit p gets list positions p, 63 - p,
+// 64 + p, 127 - p, ..., about the same total work on every unit.  This pays
+// when the resident set holds most of the grid (the d = 64 forward, 4 per
+// unit); later workgroups keep the longest-first order, which the in-order
+// dispatch balances by itself (with 2 per unit the backward passes measured
+// slower with the snake).
 constexpr int kGroupTiles = 128;
+constexpr int kXcdCUs = 32;  // compute units per XCD
 __device__ __forceinline__ void map_block(int bid, int BH, int T, bool heavy_high, int* bh,
-                                          int* tile) {
+                                          int* tile, int snake_rounds = 0) {
     int heads = BH, base = 0, li = bid;
     if ((BH & 7) == 0) {
         heads = BH >> 3;
         base = (bid & 7) * heads;
         li = bid >> 3;
+        const int q = li / kXcdCUs, p = li - q * kXcdCUs;
+        if ((q & 1) && q < snake_rounds && q < (heads * T) / kXcdCUs)
+            li = q * kXcdCUs + (kXcdCUs - 1 - p);
     }
     const int hg = min(heads, max(1, (kGroupTiles + T - 1) / T));
     const int group = li / (hg * T);

@@ -290,7 +290,7 @@ __global__ __launch_bounds__(kThreads, GPA_FWD16_OCC) void fwd_sbs_q16_kernel(
 
     const int T = (Nmax + kTile - 1) / kTile;  // tiles of the longest problem
     int bh, tile;
-    map_block(blockIdx.x, BH, T, causal != 0, &bh, &tile);
+    map_block(blockIdx.x, BH, T, causal != 0, &bh, &tile, GPA_FWD16_OCC);
     const SeqRows sr = seq_rows(cu, cu_k, bh, Nmax, Nkmax, G, Hq, total, total_k);
     const int N = sr.nq, Nk = sr.nk;
     if (tile * kTile >= N) return;  // a shorter sequence has no such tile
