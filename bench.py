@@ -32,8 +32,11 @@ PEAK_HBM_GBS = 8000.0
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=10)
+    # The part needs some tens of milliseconds of sustained load to reach its
+    # steady clock; 200 warmup steps (~45 ms at the default size) get there,
+    # and 200 timed steps take ~45 ms.
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=200)
     p.add_argument("--mode", default="gproj", choices=["plain", "gproj_q", "gproj"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-accuracy", action="store_true")
