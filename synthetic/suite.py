@@ -91,6 +91,15 @@ class SuiteCase:
     def max_seqlen_k(self) -> int:
         return int(max(self.key_lens))
 
+    def unseen_keys(self) -> np.ndarray:
+        """Boolean [total_k]: keys no query sees (those of sequences without
+        queries; with causal the last query of a sequence sees all its keys)."""
+        e = np.zeros(self.total_k, dtype=bool)
+        for a, nq, nk in zip(self.cu_k[:-1], self.lens, self.key_lens):
+            if nq == 0:
+                e[a:a + nk] = True
+        return e
+
     def empty_rows(self) -> np.ndarray:
         """Boolean [total]: queries that see no key (no keys in their
         sequence, or, with causal, the first nq - nk queries)."""
@@ -188,6 +197,7 @@ def _cases():
         lens_k=(128, 104))
     add("non-causal sequence without keys", "unequal query/key", (10, 20), causal=False,
         lens_k=(30, 0))
+    add("sequence without queries", "unequal query/key", (0, 30, 7), lens_k=(50, 30, 70))
     return C
 
 

@@ -38,16 +38,22 @@ def test_autograd_matches_direct_calls(gpa, mode):
         assert np.array_equal(G.bits(a), G.bits(b))
 
 
-def test_autograd_varlen_matches_direct_calls(gpa):
-    case = suite.CASES[8]
+@pytest.mark.parametrize("name", ["unequal lengths mixed", "more queries than keys"])
+def test_autograd_varlen_matches_direct_calls(gpa, name):
+    case = next(c for c in suite.CASES if c.name == name)
     x = suite.make_case(case)
     G.log(f"autograd varlen: case {case.index:03d} {case.name}")
     q, k, v, u = (G.to_dev(x[n]) for n in ("q", "k", "v", "do"))
     cu = torch.tensor(case.cu, dtype=torch.int32, device="cuda:0")
-    o_ref, lse = gpa.attn_fwd_varlen(q, k, v, cu, case.max_seqlen, True, case.scale)
-    ref = gpa.attn_bwd_varlen(q, k, v, o_ref, lse, u, cu, case.max_seqlen, "gproj", True, case.scale)
+    kw = {}
+    if case.cross:
+        kw = dict(cu_seqlens_k=torch.tensor(case.cu_k, dtype=torch.int32, device="cuda:0"),
+                  max_seqlen_k=case.max_seqlen_k)
+    o_ref, lse = gpa.attn_fwd_varlen(q, k, v, cu, case.max_seqlen, True, case.scale, **kw)
+    ref = gpa.attn_bwd_varlen(q, k, v, o_ref, lse, u, cu, case.max_seqlen, "gproj", True,
+                              case.scale, **kw)
     qa, ka, va = (t.clone().requires_grad_(True) for t in (q, k, v))
-    o = gpa.attention_varlen(qa, ka, va, cu, case.max_seqlen, True, case.scale, "gproj")
+    o = gpa.attention_varlen(qa, ka, va, cu, case.max_seqlen, True, case.scale, "gproj", **kw)
     o.backward(u)
     torch.cuda.synchronize()
     assert np.array_equal(G.bits(o.detach()), G.bits(o_ref))

@@ -146,6 +146,11 @@ def test_suite_case(gpa, case):
         for n in ("m", "rho", "lam"):
             assert np.all(out["gproj"][n][:, empty] == 0.0), n
     assert np.all(np.isfinite(out["LSE"][:, ~empty]))
+    # keys no query sees get dK = dV = 0 exactly
+    unseen = case.unseen_keys()
+    if unseen.any():
+        for m in MODES:
+            assert np.all(out[m]["dK"][:, unseen] == 0.0) and np.all(out[m]["dV"][:, unseen] == 0.0), m
     if case.name == "singleton":
         assert np.all(out["gproj"]["dQ"] == 0.0)
         assert np.abs(out["gproj"]["dK"]).max() <= ZERO_ABS

@@ -59,5 +59,8 @@ def test_unequal_query_key_cases():
     assert none.empty_rows().sum() == 20 + 5
     nc = next(c for c in cross if c.name == "non-causal sequence without keys")
     assert nc.empty_rows().tolist() == [False] * 10 + [True] * 20
+    nq0 = next(c for c in cross if c.name == "sequence without queries")
+    assert nq0.unseen_keys().tolist() == [True] * 50 + [False] * 100
+    assert not any(c.unseen_keys().any() for c in suite.CASES if c.name != nq0.name and c.cross)
     # square cases have no empty rows unless a sequence is empty
     assert not any(c.empty_rows().any() for c in suite.CASES if not c.cross)
