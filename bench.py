@@ -144,6 +144,27 @@ def main():
         bwd_ms[m] = timed(lambda: gpa.attn_bwd(q, k, v, o, lse, u, m, w.causal, w.scale,
                                                workspace=ws[m]), args.steps)
     fwd_ms = timed(lambda: gpa.attn_fwd(q, k, v, w.causal, w.scale), args.steps)
+
+    # Per-call distribution (p10 / median / p90 ms): each call bracketed by its
+    # own pair of events, so each figure carries a few microseconds of event
+    # overhead that the K-step means above do not.
+    def percentiles(fn, iters):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(iters)]
+        torch.cuda.synchronize()
+        for a, b in ev:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        t = np.sort(np.array([a.elapsed_time(b) for a, b in ev]))
+        return [round(float(np.percentile(t, p)), 5) for p in (10, 50, 90)]
+
+    per_call = {"fwd": percentiles(lambda: gpa.attn_fwd(q, k, v, w.causal, w.scale), args.steps)}
+    for m in gpa.MODES:
+        per_call["bwd_" + m] = percentiles(
+            lambda: gpa.attn_bwd(q, k, v, o, lse, u, m, w.causal, w.scale, workspace=ws[m]),
+            args.steps)
     # The FP32-arithmetic attention (forward + backward in one call, BF16 I/O):
     # the accuracy-class baseline, timed beside the BF16 path.
     for _ in range(2):
@@ -201,6 +222,7 @@ def main():
         "kernels_ms": {k2: round(v2, 5) for k2, v2 in kern.items()},
         "fwd_ms": round(fwd_ms, 5),
         "bwd_ms": {m: round(t, 5) for m, t in bwd_ms.items()},
+        "per_call_ms_p10_p50_p90": per_call,
         "gproj_bwd_overhead_vs_plain_pct": round(100.0 * (bwd_ms["gproj"] / bwd_ms["plain"] - 1), 2),
         "gproj_q_bwd_overhead_vs_plain_pct": round(100.0 * (bwd_ms["gproj_q"] / bwd_ms["plain"] - 1), 2),
         "fp32_attn_fwd_bwd_ms": round(fp32_ms, 5),
