@@ -108,6 +108,46 @@ def _passes(a, t):
 def test_suite_case(gpa, case):
     G.log(f"suite case {case.index:03d} {case.name}: lens={case.lens[:6]}{'...' if len(case.lens) > 6 else ''} "
           f"packed={case.packed} causal={case.causal} Hq={case.Hq} Hkv={case.Hkv} d={case.d}")
+    check_case(gpa, case)
+
+
+def random_packed_case(r: int) -> suite.SuiteCase:
+    """Seeded random packed layout: 1-5 sequences of 0-259 queries, keys of
+    the same or their own lengths, causal or not, d = 64 or 128, grouped or
+    multi-head; lengths near tile edges are drawn often."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([424242, r])))
+    nseq = int(rng.integers(1, 6))
+
+    def lengths():
+        edge = rng.choice([0, 1, 63, 64, 65, 127, 128, 129, 191, 192, 193], nseq)
+        free = rng.integers(0, 260, nseq)
+        return tuple(int(x) for x in np.where(rng.random(nseq) < 0.4, edge, free))
+
+    lens = lengths()
+    while max(lens) == 0:
+        lens = lengths()
+    lens_k = ()
+    if rng.random() < 0.6:
+        lens_k = lengths()
+        while max(lens_k) == 0:
+            lens_k = lengths()
+    Hq, Hkv = [(4, 2), (2, 2), (4, 1), (8, 2)][int(rng.integers(0, 4))]
+    return suite.SuiteCase(1000 + r, f"random packed {r}", "random", lens, packed=True,
+                           causal=bool(rng.random() < 0.7), Hq=Hq, Hkv=Hkv,
+                           d=128 if rng.random() < 0.25 else 64, lens_k=lens_k)
+
+
+@pytest.mark.parametrize("r", range(16))
+def test_random_packed_layout(gpa, r):
+    """Seeded random packings (unequal query/key counts, empty sequences and
+    rows, tile-edge lengths) checked like the suite's cases."""
+    case = random_packed_case(r)
+    G.log(f"random packed {r}: lens={case.lens} lens_k={case.lens_k} causal={case.causal} "
+          f"Hq={case.Hq} Hkv={case.Hkv} d={case.d}")
+    check_case(gpa, case)
+
+
+def check_case(gpa, case):
     x = suite.make_case(case)
     ex = oracle.exact_varlen(x["q"], x["k"], x["v"], x["do"], case.cu, case.causal, case.scale,
                              cu_seqlens_k=case.cu_k)
