@@ -205,6 +205,30 @@ def test_tiny_workload(gpa, seed):
     assert mass.min() > 0.99 and mass.max() < 1.01
 
 
+# ------------------------------------------------------- key-bias sweep
+
+def test_key_bias_sweep(gpa):
+    """Theorem 4.2: the plain backward's dQ error grows linearly in the common
+    key offset relative to the key spread, while GProj's does not move.  Sweep
+    the per-channel key bias spread 0, 4, 16, 64 at N = 1024 (two heads)."""
+    errs = {}
+    for kb in (0.0, 4.0, 16.0, 64.0):
+        w = S.Workload("bias sweep", 1, 2, 1024, 64, k_bias_std=kb, do_std=1.0)
+        x = S.make_inputs(w, 5150)
+        out = run_all(gpa, x, True, w.scale)
+        ex = oracle.exact(x["q"], x["k"], x["v"], x["do"], True, w.scale)
+        e = errors_vs_exact(out, ex)
+        check_accuracy_gates(e, f"key bias {kb}", blowup_ratio=0)
+        errs[kb] = (e["plain"]["dQ"], e["gproj"]["dQ"])
+    G.log("[key bias sweep] plain / gproj dQ %: " +
+          ", ".join(f"{kb:g}: {p:.3f} / {g:.3f}" for kb, (p, g) in errs.items()))
+    plain = [errs[kb][0] for kb in (0.0, 4.0, 16.0, 64.0)]
+    assert all(a < b for a, b in zip(plain, plain[1:])), plain
+    assert 3.0 <= plain[3] / plain[2] <= 6.0, plain          # linear: 64 / 16 = 4
+    assert all(g <= 0.5 for _, g in errs.values())
+    assert max(g for _, g in errs.values()) <= 1.2 * min(g for _, g in errs.values())
+
+
 # --------------------------------------------------------- ragged shapes
 
 RAGGED = [(1, 1, 1, 64, True), (1, 2, 17, 64, True), (2, 1, 65, 128, True),
