@@ -208,9 +208,10 @@ def test_tiny_workload(gpa, seed):
 # ------------------------------------------------------- key-bias sweep
 
 def test_key_bias_sweep(gpa):
-    """Theorem 4.2: the plain backward's dQ error grows linearly in the common
-    key offset relative to the key spread, while GProj's does not move.  Sweep
-    the per-channel key bias spread 0, 4, 16, 64 at N = 1024 (two heads)."""
+    """The theorem on forward repair versus projection (Section 4): the plain
+    backward's dQ error grows linearly in the common key offset relative to
+    the key spread, while GProj's does not move.  Sweep the per-channel key
+    bias spread 0, 4, 16, 64 at N = 1024 (two heads)."""
     errs = {}
     for kb in (0.0, 4.0, 16.0, 64.0):
         w = S.Workload("bias sweep", 1, 2, 1024, 64, k_bias_std=kb, do_std=1.0)
