@@ -32,7 +32,7 @@ def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--steps", type=int, default=10, help="timed steps per mode and round")
     p.add_argument("--warmup", type=int, default=3)
-    p.add_argument("--rounds", type=int, default=3)
+    p.add_argument("--rounds", type=int, default=7)
     p.add_argument("--layers", type=int, default=24)
     p.add_argument("--seq", type=int, default=4096)
     return p.parse_args()
@@ -143,7 +143,11 @@ def main():
             e1.record()
             torch.cuda.synchronize()
             times[m].append(e0.elapsed_time(e1) / args.steps)
-    ms = {m: sorted(t)[len(t) // 2] for m, t in times.items()}
+    # The step mixes hundreds of PyTorch launches with the attention kernels
+    # and varies by several percent from round to round; the fastest of the
+    # interleaved rounds is the stable figure (the median is reported too).
+    ms = {m: min(t) for m, t in times.items()}
+    med = {m: sorted(t)[len(t) // 2] for m, t in times.items()}
     # attention kernel time inside one gproj step
     set_mode("gproj")
     gpa.profile_enable(True)
@@ -158,6 +162,7 @@ def main():
         "unit": "ms", "higher_is_better": False, "data": "synthetic",
         "params": nparams, "layers": args.layers, "seq": args.seq,
         "ms_per_step": {m: round(v, 3) for m, v in ms.items()},
+        "ms_per_step_median": {m: round(v, 3) for m, v in med.items()},
         "ms_per_step_rounds": {m: [round(x, 3) for x in v] for m, v in times.items()},
         "gproj_step_overhead_vs_plain_pct": round(100 * (ms["gproj"] / ms["plain"] - 1), 2),
         "gproj_q_step_overhead_vs_plain_pct": round(100 * (ms["gproj_q"] / ms["plain"] - 1), 2),
