@@ -22,6 +22,9 @@ Contents
                         sequence its own attention problem; separate query
                         and key lengths with the causal diagonal aligned at
                         the end, empty rows).
+  sampled               exact rows (O, LSE, dQ) and last keys (dK, dV) of one
+                        long causal head, each from its own row softmaxes, for
+                        sizes the full oracle cannot take.
   rel_l2                the paper's metric: 100 ||G_hat - G64||_2 / ||G64||_2
                         over a full tensor (appendix "Reference and metric").
 """

@@ -205,6 +205,45 @@ def test_tiny_workload(gpa, seed):
     assert mass.min() > 0.99 and mass.max() < 1.01
 
 
+# ------------------------------------- long heads, sampled exact outputs
+
+@pytest.mark.parametrize("N,d", [(262144, 64), (131035, 128)])
+def test_long_head_sampled_outputs(gpa, N, d):
+    """One causal head of 2^18 tokens (d = 64) and of 2^17 - 37 tokens
+    (d = 128), far beyond the full oracle: O, LSE and dQ at sampled rows and
+    dK, dV at the last 8 keys against oracle.sampled, to the same gates; mode
+    identities on the whole tensors."""
+    from oracle import sampled
+    w = S.Workload("long head", 1, 1, N, d, k_bias_std=8.0, do_std=0.01)
+    x = S.make_inputs(w, 9100 + d)
+    G.log(f"long head N={N} d={d}")
+    q, k, v, u = (G.to_dev(x[n]) for n in ("q", "k", "v", "do"))
+    o, lse = gpa.attn_fwd(q, k, v, True, w.scale)
+    res = {m: gpa.attn_bwd(q, k, v, o, lse, u, m, True, w.scale) for m in MODES}
+    torch.cuda.synchronize()
+    assert torch.equal(res["gproj"][0], res["gproj_q"][0])
+    assert torch.equal(res["gproj_q"][1], res["plain"][1])
+    assert torch.equal(res["gproj"][2], res["plain"][2])
+    rows = [0, 1, 63, 64, 4095, N // 2, N - 65, N - 1]
+    h = lambda n: x[n][0, 0]  # noqa: E731
+    ref = sampled.exact_rows(h("q"), h("k"), h("v"), h("do"), rows, w.scale)
+    keys = sampled.exact_last_keys(h("q"), h("k"), h("v"), h("do"), 8, w.scale)
+    idx = torch.tensor(rows, device=q.device)
+    e = {"O": G.rel_l2(G.to_host(o[0, 0, idx]), ref["O"])}
+    lse_err = float(np.abs(G.to_host(lse[0, 0, idx]) - ref["LSE"]).max())
+    for m in MODES:
+        dq, dk, dv = res[m]
+        e[m] = (G.rel_l2(G.to_host(dq[0, 0, idx]), ref["dQ"]),
+                G.rel_l2(G.to_host(dk[0, 0, N - 8:]), keys["dK"]),
+                G.rel_l2(G.to_host(dv[0, 0, N - 8:]), keys["dV"]))
+    G.log(f"[long head N={N} d={d}] O {e['O']:.4f}% LSE abs {lse_err:.2e} " +
+          " ".join(f"{m} dQ/dK/dV {a:.3f}/{b:.3f}/{c:.3f}" for m, (a, b, c) in
+                   ((m, e[m]) for m in MODES)))
+    assert e["O"] <= 0.5
+    assert lse_err <= 1e-4 * max(1.0, float(np.abs(ref["LSE"]).max()))
+    assert all(x_ <= 1.0 for x_ in e["gproj"]), e["gproj"]
+
+
 # ------------------------------------------------------- key-bias sweep
 
 def test_key_bias_sweep(gpa):

@@ -470,3 +470,29 @@ def test_packed_oracle_separate_query_key_lengths(causal):
     fd = float((Lp - Lm) / (2 * hh))
     an = float(sum(np.sum(g * dd) for g, dd in zip((ex["dQ"], ex["dK"], ex["dV"]), dirs)))
     assert abs(fd - an) <= 1e-10 * max(1.0, abs(an))
+
+
+@pytest.mark.parametrize("kbias", [0.0, 16.0])
+def test_sampled_rows_and_keys_match_full_oracle(kbias):
+    """oracle.sampled (numpy, per row / per key) against the full C oracle on a
+    causal head of 300 tokens: rows at the start, tile edges and the end, and
+    the last 9 keys."""
+    from oracle import sampled
+    rng = np.random.default_rng(31)
+    N, d = 300, 64
+    q = rng.standard_normal((N, d))
+    k = rng.standard_normal((N, d)) + kbias * rng.standard_normal(d)
+    v = rng.standard_normal((N, d))
+    u = rng.standard_normal((N, d))
+    alpha = 0.125
+    ex = oracle.exact(q[None], k[None], v[None], u[None], True, alpha)
+    rows = [0, 1, 63, 64, 150, 299]
+    r = sampled.exact_rows(q, k, v, u, rows, alpha)
+    for name in ("O", "dQ"):
+        ref = ex[name][0][rows]
+        assert np.abs(r[name] - ref).max() <= 1e-12 * max(1.0, np.abs(ref).max()), name
+    assert np.abs(r["LSE"] - ex["LSE"][0][rows]).max() <= 1e-12 * max(1.0, np.abs(ex["LSE"]).max())
+    kk = sampled.exact_last_keys(q, k, v, u, 9, alpha)
+    for name in ("dK", "dV"):
+        ref = ex[name][0][N - 9:]
+        assert np.abs(kk[name] - ref).max() <= 1e-12 * max(1.0, np.abs(ref).max()), name
