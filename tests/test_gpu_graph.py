@@ -3,7 +3,8 @@ they only enqueue kernels on the caller's stream, with no allocation, memset
 or synchronisation of their own.  A captured forward + backward, replayed
 several times with other eager work and synchronisations between replays,
 gives bitwise the eager results on every replay (dense grouped-query and
-packed layouts, all three backward modes)."""
+packed layouts, all three backward modes).  Calls on concurrent side streams
+give the default stream's results."""
 import numpy as np
 import pytest
 import torch
@@ -94,3 +95,38 @@ def test_graph_packed(gpa):
                                              True, case.scale, workspace=ws, **kw)]
 
     _capture_and_check(step, lambda: noise_in.mul_(0.9999).sum())
+
+
+def test_calls_on_side_streams(gpa):
+    """Every call is enqueued on the caller's current stream: two problems run
+    concurrently on two side streams (each with its own workspace) give
+    bitwise the results of the same calls on the default stream."""
+    w = S.WORKLOADS[2].with_shape(H=2, N=1500)
+    xs = [S.make_inputs(w, s) for s in (71, 72)]
+    G.log("side streams: h2 N=1500, two problems")
+    dev = torch.device("cuda:0")
+    ins = [[G.to_dev(x[n]) for n in ("q", "k", "v", "do")] for x in xs]
+    B, H, N, d = ins[0][0].shape
+
+    def run(q, k, v, u, ws):
+        o, lse = gpa.attn_fwd(q, k, v, True, w.scale)
+        return [o, lse, *gpa.attn_bwd(q, k, v, o, lse, u, "gproj", True, w.scale, workspace=ws)]
+
+    wss = [torch.empty(gpa.attn_bwd_workspace_bytes(B, H, N, d, "gproj"), dtype=torch.uint8,
+                       device=dev) for _ in range(2)]
+    ref = [run(*ins[i], wss[i]) for i in range(2)]
+    ref = [[t.clone() for t in r] for r in ref]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream() for _ in range(2)]
+    for s in streams:
+        s.wait_stream(torch.cuda.current_stream())
+    outs = []
+    for i, s in enumerate(streams):
+        with torch.cuda.stream(s):
+            outs.append(run(*ins[i], wss[i]))
+    for s in streams:
+        torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    for r, o in zip(ref, outs):
+        for a, b in zip(r, o):
+            assert torch.equal(a, b)
