@@ -283,6 +283,26 @@ def main():
                 acc[m] = {n: round(oracle.rel_l2(host(t), ex[n]), 4)
                           for n, t in (("O", oo), ("dQ", dq), ("dK", dk), ("dV", dv))}
             out["rel_l2_pct_vs_fp64"] = acc
+            # Context: the regime of the paper's captures (near one-hot rows at
+            # a logit scale of ~10^4, large common key offset), where the
+            # forward's exponent rounding matters: FA3 (FMA forward + plain),
+            # FA3-SBS (plain) and GProj, N = 1024, two heads.
+            ws_ = S.Workload("sharp regime", 1, 2, 1024, 64, q_std=3000.0, k_bias_std=64.0,
+                             do_std=1.0)
+            xs_ = S.make_inputs(ws_, 777)
+            qs_, ks_, vs_, us_ = (to_dev(xs_[n]) for n in ("q", "k", "v", "do"))
+            exs_ = oracle.exact(xs_["q"], xs_["k"], xs_["v"], xs_["do"], True, ws_.scale)
+            sharp = {}
+            for name, fwd, m in (("fa3_fma_plain", gpa.attn_fwd_fma, "plain"),
+                                 ("plain", gpa.attn_fwd, "plain"), ("gproj", gpa.attn_fwd, "gproj")):
+                oo, ll = fwd(qs_, ks_, vs_, True, ws_.scale)
+                dq, dk, dv = gpa.attn_bwd(qs_, ks_, vs_, oo, ll, us_, m, True, ws_.scale)
+                torch.cuda.synchronize()
+                hs = lambda t: t.float().cpu().numpy().astype(np.float64)  # noqa: E731
+                sharp[name] = {n: round(oracle.rel_l2(hs(t), exs_[n]), 4)
+                               for n, t in (("O", oo), ("dQ", dq), ("dK", dk), ("dV", dv))}
+            out["rel_l2_pct_sharp_regime"] = {"workload": "q_std 3000, k_bias_std 64, 2 heads, "
+                                                          "N 1024, d 64, causal", **sharp}
     if args.calibrate_copy:
         # A plain device copy of known size: FETCH_SIZE / WRITE_SIZE of this
         # kernel calibrate the counters of the attention kernels.  The source
