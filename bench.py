@@ -301,6 +301,10 @@ def main():
                 hs = lambda t: t.float().cpu().numpy().astype(np.float64)  # noqa: E731
                 sharp[name] = {n: round(oracle.rel_l2(hs(t), exs_[n]), 4)
                                for n, t in (("O", oo), ("dQ", dq), ("dK", dk), ("dV", dv))}
+            fo, _, fdq, fdk, fdv = gpa.fp32_attn(qs_, ks_, vs_, us_, True, ws_.scale)
+            torch.cuda.synchronize()
+            sharp["fp32"] = {n: round(oracle.rel_l2(hs(t), exs_[n]), 4)
+                             for n, t in (("O", fo), ("dQ", fdq), ("dK", fdk), ("dV", fdv))}
             out["rel_l2_pct_sharp_regime"] = {"workload": "q_std 3000, k_bias_std 64, 2 heads, "
                                                           "N 1024, d 64, causal", **sharp}
     if args.calibrate_copy:

@@ -265,10 +265,17 @@ def test_fa3_ordering_in_the_sharp_regime(gpa):
             torch.cuda.synchronize()
             e[fwd_name, m] = {n: G.rel_l2(G.to_host(t), ex[n])
                               for n, t in (("O", o), ("dQ", dq), ("dK", dk), ("dV", dv))}
+    fo, _, fdq, fdk, fdv = gpa.fp32_attn(q, k, v, u, True, w.scale)
+    torch.cuda.synchronize()
+    e["fp32", "-"] = {n: G.rel_l2(G.to_host(t), ex[n])
+                      for n, t in (("O", fo), ("dQ", fdq), ("dK", fdk), ("dV", fdv))}
     G.log("[sharp regime] " + " | ".join(
         f"{f}+{m}: " + "/".join(f"{e[f, m][n]:.3f}" for n in ("O", "dQ", "dK", "dV"))
         for f, m in e))
-    fa3, sbs, gp = e["fma", "plain"], e["sbs", "plain"], e["sbs", "gproj"]
+    fa3, sbs, gp, f32 = e["fma", "plain"], e["sbs", "plain"], e["sbs", "gproj"], e["fp32", "-"]
+    # GProj's dQ and dK sit in the FP32 baseline's accuracy class here too (the
+    # paper: GProj 0.342 / 0.371 %, fused FP32 0.385 / 0.371 %)
+    assert gp["dQ"] <= 1.5 * f32["dQ"] and gp["dK"] <= 1.5 * f32["dK"]
     assert fa3["O"] > 2.0 * sbs["O"]
     assert fa3["dQ"] > 2.0 * sbs["dQ"] and sbs["dQ"] > 10.0 * gp["dQ"]
     assert fa3["dK"] > 2.0 * sbs["dK"] and sbs["dK"] > gp["dK"]
