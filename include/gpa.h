@@ -32,7 +32,8 @@
  *   Stream   a hipStream_t passed as void* (NULL = the null stream).  All work
  *            is enqueued on it asynchronously; the library never synchronises,
  *            never allocates or frees device memory, and fully overwrites every
- *            output.
+ *            output.  Calls only enqueue kernels, so they can be captured into
+ *            HIP graphs.
  *   Errors   arguments are validated before anything is launched; on error no
  *            work is enqueued and nothing is written.  GPA_EHIP reports a launch
  *            failure (text in gpa_last_error(), per thread).  No C++ exception
