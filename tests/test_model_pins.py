@@ -9,6 +9,7 @@ the synthetic offset sweep floor the paper reports.
 """
 import json
 import os
+import sys
 
 import numpy as np
 import pytest
@@ -64,11 +65,53 @@ def _witness(golden_dir):
     return w, q, k, v, u
 
 
+def _witness_from_printed(pb):
+    """Witness-row dQ from the paper's printed values alone, in exact
+    rationals: A = sum_j t_j k_j with the printed BF16 t, B = sum_j r_j k_j
+    with r = BF16(p) = p (every printed p is 1/4, a BF16 value), lambda =
+    rho / m with the printed rho and m = sum r = 1; plain dq = BF16(alpha A),
+    GProj dq = BF16(fl32[alpha (A - lambda B)]) (every intermediate here is
+    exact in FP32)."""
+    from fractions import Fraction as F
+    import _sbs_rational as R
+    t = [F(x) for x in pb["t_bf16"]]
+    r = [F(x) for x in pb["p"]]
+    k = [[F(x) for x in row] for row in pb["k"]]
+    alpha = F(pb["alpha"])
+    A = [sum(t[j] * k[j][c] for j in range(4)) for c in range(2)]
+    B = [sum(r[j] * k[j][c] for j in range(4)) for c in range(2)]
+    lam = F(pb["rho"]) / sum(r)
+    before = [alpha * (A[c] - lam * B[c]) for c in range(2)]
+    assert all(R.rn32(x) == x for x in A + B + before)  # exact in FP32
+    return {"A": [float(x) for x in A], "B": [float(x) for x in B], "lambda": float(lam),
+            "gproj_dq_before_cast": [float(x) for x in before],
+            "plain_dq_bf16": [float(R.bf16_nearest(R.rn32(alpha * A[c]))) for c in range(2)],
+            "gproj_dq_bf16": [float(R.bf16_nearest(R.rn32(x))) for x in before]}
+
+
+def test_witness_derived_values_match_the_fixture(golden_dir):
+    """The fixture's oracle-written block (tests/golden/derive_witness.py)
+    equals both what that script derives now and the exact-rational values
+    computed from the printed quantities alone."""
+    sys.path.insert(0, golden_dir)
+    import derive_witness
+    with open(os.path.join(golden_dir, "witness_minus24.json")) as f:
+        w = json.load(f)
+    stored = w["derived_by_oracle"]
+    fresh = derive_witness.derive(w["printed_by_paper"])
+    for key, val in fresh.items():
+        assert stored[key] == val, key
+    hand = _witness_from_printed(w["printed_by_paper"])
+    for key, val in hand.items():
+        assert stored[key] == val, key
+    assert stored["exact_dq"][0] == w["printed_by_paper"]["exact_dq_first_coordinate"]
+
+
 def test_witness_through_the_model(golden_dir):
     """Plain contracts the cast operand and returns -24; GProj returns exactly 0
     (Section 3.4, appendix A, Section 5.2 'on the four-key example ... exactly zero')."""
     w, q, k, v, u = _witness(golden_dir)
-    pb, hand = w["printed_by_paper"], w["derived_by_hand_from_printed_values"]
+    pb, hand = w["printed_by_paper"], _witness_from_printed(w["printed_by_paper"])
     alpha = pb["alpha"]
     out = {}
     for mode in M.MODES:
@@ -221,3 +264,101 @@ def test_historical_fma_argument_is_the_rounding_error():
                 assert np.array_equal(o, v)
             want = M.bf16_round((v * M.bf16_round(z)) / z)
             assert np.array_equal(o, want)
+
+
+# ------------------------------------------------ the SBS forward, pinned
+
+def test_sbs_forward_single_key_rows_are_exact():
+    """Appendix 'Prescribed FMA cases': query coordinates c * 2^k (c in
+    {3, 5, 7}, k = 0..15), key coordinates 1, lengths 1 and 128.  The first
+    causal row sees one key, so the subtract-before-scale forward must give
+    z = 1 exactly and o_0 = v_0 bit for bit, and LSE_0 = fl32(alpha x_0), in
+    all 96 cases."""
+    rng = np.random.default_rng(0)
+    d = 64
+    for N in (1, 128):
+        for cval in (3, 5, 7):
+            for kexp in range(16):
+                q = np.full((N, d), cval * 2.0 ** kexp, np.float32)
+                k = np.ones((N, d), np.float32)
+                v = rng.integers(-4, 5, (N, d)).astype(np.float32)
+                O, LSE, x = M.sbs_forward(q, k, v, True, 0.125)
+                assert np.array_equal(O[0], v[0]), (N, cval, kexp)
+                x0 = np.float32(64 * cval * 2.0 ** kexp)
+                assert x[0, 0] == x0
+                assert LSE[0] == np.float32(np.float32(0.125) * x0), (N, cval, kexp)
+
+
+def test_sbs_forward_rounding_order_against_exact_rationals():
+    """Eq. gproj-forward evaluated in exact rational arithmetic (each FP32
+    operation rounded to nearest once, exp2 and ln to 60 digits) on a row
+    whose logits are ~4.2e6: the model's O and LSE equal the
+    subtract-then-scale evaluation bit for bit, while the scale-then-subtract
+    order and the historical FMA give different outputs on this row (so a
+    model that swapped the order would fail here)."""
+    import _sbs_rational as R
+    q, k, v, x = R.rounding_order_row()
+    for causal in (False, True):
+        O, LSE, xm = M.sbs_forward(q, k, v, causal, 0.125)
+        assert [np.float32(t) for t in xm[-1, :len(x)]] == x  # logits exact in FP32
+        last = len(x) - 1
+        o_ref, lse_ref, _ = R.sbs_row(x, v, 0.125, "sbs")
+        assert np.array_equal(O[last], o_ref)
+        assert LSE[last] == lse_ref
+    o_sts, _, _ = R.sbs_row(x, v, 0.125, "scale_then_subtract")
+    o_fma, _, _ = R.sbs_row(x, v, 0.125, "fma")
+    assert np.count_nonzero(R.bf16_ulps(o_sts, o_ref) >= 2) >= 10
+    assert np.count_nonzero(R.bf16_ulps(o_fma, o_ref) >= 2) >= 10
+    # rows with a single visible key (causal row 0) are exact in every order
+    O, _, _ = M.sbs_forward(q, k, v, True, 0.125)
+    assert np.array_equal(O[0], v[0])
+
+
+def test_historical_fma_one_key_outer_formula_in_rationals():
+    """Eq. historical-one-key, o = BF16(fl32(BF16(z) v / z)), checked with the
+    FP32 product and quotient evaluated exactly and rounded once each, for
+    the 48 single-key logits 64 c 2^k and a spread of value rows."""
+    import _sbs_rational as R
+    from fractions import Fraction
+    a = np.float32(np.float32(0.125) * np.float32(M.LOG2E))
+    rng = np.random.default_rng(5)
+    for c in (3, 5, 7):
+        for kexp in range(16):
+            x = np.float32(64 * c * 2 ** kexp)
+            err = Fraction(float(x)) * Fraction(float(a)) - Fraction(float(np.float32(x * a)))
+            z = R.exp2_rn32(R.rn32(err))
+            zb = R.bf16_nearest(z)
+            v = np.array([R.bf16_nearest(t) for t in rng.standard_normal(16) * 4], np.float32)
+            want = np.array([R.bf16_nearest(R.rn32(Fraction(float(R.rn32(Fraction(float(zb)) *
+                                                                        Fraction(float(vi)))))
+                                                   / Fraction(float(z))))
+                             for vi in v], np.float32)
+            assert np.array_equal(M.historical_fma_one_key(x, 0.125, v), want), (c, kexp)
+
+
+def test_row_and_tile_bounds_on_the_model_and_planted_defects():
+    """The per-row / per-tile parity bounds used at full size: the BF16 model
+    of Algorithm 1 meets them on the reference recipe (N = 1024, two heads),
+    and a planted defect in its output -- one 64-row tile scaled by 1.07, or
+    one row by 1.6 -- breaks them."""
+    import _rowtile as RT
+    w = S.WORKLOADS[2].with_shape(H=2, N=1024)
+    x = S.make_inputs(w, 11)
+    ex = oracle.exact(x["q"], x["k"], x["v"], x["do"], True, w.scale)
+    outs = {}
+    for h in range(2):
+        q, k, v, u = (S.bf16_bits_to_f32(x[n][0, h]) for n in ("q", "k", "v", "do"))
+        O, L, dq, dk, dv, st = M.forward_backward(q, k, v, u, True, w.scale, "gproj")
+        for n, a in zip(("O", "dQ", "dK", "dV"), (O, dq, dk, dv)):
+            outs.setdefault(n, []).append(a)
+    for n, arrs in outs.items():
+        got = np.stack(arrs)[None].astype(np.float64)
+        RT.check(got, ex[n], n)
+        bad = got.copy()
+        bad[0, 1, 640:704] *= 1.07
+        with pytest.raises(AssertionError):
+            RT.check(bad, ex[n], n)
+        bad = got.copy()
+        bad[0, 0, 300] *= 1.6
+        with pytest.raises(AssertionError):
+            RT.check(bad, ex[n], n)
