@@ -83,14 +83,19 @@ __device__ __forceinline__ void dq_probs(const f32x4 (&s)[2], const f32x4 (&dp)[
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            float P = fexp2(fmaf(s[kb][i], c, -lse2));
+            const float P = fexp2(fmaf(s[kb][i], c, -lse2));
+            const __bf16 t = to_bf16(P * (dp[kb][i] - Di)), r = to_bf16(P);
             if constexpr (MASK) {
+                // select, not multiply: a masked pair contributes exactly 0
+                // whatever its logit, dP or LDS row held
                 const int key = key0 + kb * 16 + 4 * g + i;
                 const bool ok = key < Nk && (!causal || key <= qrow + off);
-                P = ok ? P : 0.f;
+                tf[kb * 4 + i] = ok ? t : (__bf16)0.0f;
+                rf[kb * 4 + i] = ok ? r : (__bf16)0.0f;
+            } else {
+                tf[kb * 4 + i] = t;
+                rf[kb * 4 + i] = r;
             }
-            tf[kb * 4 + i] = to_bf16(P * (dp[kb][i] - Di));
-            rf[kb * 4 + i] = to_bf16(P);
         }
 }
 
@@ -391,10 +396,17 @@ __device__ __forceinline__ void dkdv_probs(const f32x4& s, const f32x4& dp, cons
                                            int off, int half, bf16x8& tf, bf16x8& rf) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        float P = fexp2(fmaf(s[i], c, -l2[i]));
-        if constexpr (MASK) P = (krow <= qb + 4 * g + i + off) ? P : 0.f;
-        tf[half * 4 + i] = to_bf16(P * (dp[i] - dd[i]));
-        rf[half * 4 + i] = to_bf16(P);
+        const float P = fexp2(fmaf(s[i], c, -l2[i]));
+        const __bf16 t = to_bf16(P * (dp[i] - dd[i])), r = to_bf16(P);
+        if constexpr (MASK) {
+            // select, not multiply: a masked pair contributes exactly 0
+            const bool ok = krow <= qb + 4 * g + i + off;
+            tf[half * 4 + i] = ok ? t : (__bf16)0.0f;
+            rf[half * 4 + i] = ok ? r : (__bf16)0.0f;
+        } else {
+            tf[half * 4 + i] = t;
+            rf[half * 4 + i] = r;
+        }
     }
 }
 

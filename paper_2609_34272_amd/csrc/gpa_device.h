@@ -131,8 +131,11 @@ __device__ __forceinline__ void lds_dma4(i32x4 desc, uint32_t m0, uint32_t voff)
 // and every lane loads the global chunk that the swizzle places in its slot.
 // No registers or LDS write instructions are involved; completion is tracked
 // by vmcnt.  The resource of a call starts at the tile's first row and ends at
-// the tensor's last row, so rows at or beyond N are range-checked away (the
-// LDS slot keeps whatever it held; callers make that harmless).
+// the tensor's last row, so rows at or beyond N are range-checked away: their
+// lanes read nothing and write zeros into their LDS slots (measured with an
+// in-bounds probe).  The kernels do not rely on that for correctness: every
+// probability of a row or key beyond the problem is exactly 0, and the masked
+// steps select (not multiply) the operands that meet those rows.
 template <int D, int NTHR = kThreads>
 struct TileDma {
     static constexpr int NWAVES = NTHR / 64;

@@ -94,8 +94,9 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
     const KeyRange kr = key_range(tile, Nk, off, causal);
     const int nkv = kr.nkv, nplain = kr.nplain;
 
-    // Rows beyond Nk are never written by the DMA: zero both buffers once so
-    // every value a product can read is finite.
+    // Zero both buffers once, so that every value a product can read is finite
+    // whatever the DMA leaves in the slots of rows beyond Nk (it writes zeros
+    // there, but the tail does not depend on it).
     {
         u32x4* z0 = reinterpret_cast<u32x4*>(&KV0[0][0]);
         u32x4* z1 = reinterpret_cast<u32x4*>(&KV1[0][0]);
@@ -250,8 +251,10 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
         const int qrow = q0w + nb * 16 + c16;
         if (qrow < N) {
             // A query that sees no key (l = 0; a visible key adds z = 1) gets
-            // O = 0 and LSE = +inf, so the backward's P is 0 on its row.
-            const bool empty = !(ltot > 0.f);
+            // O = 0 and LSE = +inf, so the backward's P is 0 on its row.  l is
+            // +0 exactly then; the test is on the bits so that a NaN row (NaN
+            // l) keeps NaN outputs whatever the compiler assumes about NaNs.
+            const bool empty = __float_as_uint(ltot) == 0u;
             uint16_t* orow = O + hoff + (size_t)qrow * D;
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb) {
@@ -414,8 +417,10 @@ __global__ __launch_bounds__(kThreads, GPA_FWD16_OCC) void fwd_sbs_q16_kernel(
     const float ltot = xor_sum(lrun);
     if (qrow < N) {
         // A query that sees no key (l = 0; a visible key adds z = 1) gets O = 0
-        // and LSE = +inf, so the backward's P is 0 on its row.
-        const bool empty = !(ltot > 0.f);
+        // and LSE = +inf, so the backward's P is 0 on its row.  l is +0 exactly
+        // then; the test is on the bits so that a NaN row (NaN l) keeps NaN
+        // outputs whatever the compiler assumes about NaNs.
+        const bool empty = __float_as_uint(ltot) == 0u;
         uint16_t* orow = O + hoff + (size_t)qrow * D;
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
