@@ -256,6 +256,24 @@ BwdLayout varlen_layout(const Varlen& v, int mode) {
     return bwd_layout_rows((size_t)v.Hq * v.total_q, (size_t)v.Hq * v.total_k,
                            (size_t)v.nseq * v.Hq, v.max_q, v.d, mode, v.Hq > v.Hkv);
 }
+// Fused FP32 baseline workspace: the saved FP32 output O32 [B,H,N,d], the
+// scaled row maximum and the inverse normaliser [B,H,N] each, and the
+// per-tile statistics the key-major pass stages ([B*H, T, 3, 64]).
+struct F32Layout {
+    size_t o32, mrow, linv, ts, total;
+};
+F32Layout f32_layout(int64_t B, int64_t H, int64_t N, int64_t d) {
+    const size_t rows = (size_t)B * H * N;
+    const size_t T = (size_t)(N + 63) / 64;
+    F32Layout L;
+    L.o32 = 0;
+    L.mrow = round_up(rows * d * 4);
+    L.linv = L.mrow + round_up(rows * 4);
+    L.ts = L.linv + round_up(rows * 4);
+    L.total = L.ts + round_up((size_t)B * H * T * 192 * 4);
+    return L;
+}
+
 }  // namespace
 
 extern "C" {
@@ -448,7 +466,7 @@ gpa_status gpa_attn_bwd_varlen(const uint16_t* Q, const uint16_t* K, const uint1
 size_t gpa_fp32_attn_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d) {
     if (B < 1 || H < 1 || N < 1 || (d != 64 && d != 128)) return 0;
     if ((double)B * H * N * d >= 2147483648.0) return 0;
-    return round_up((size_t)B * H * N * d * 4) + round_up((size_t)B * H * N * 4);
+    return f32_layout(B, H, N, d).total;
 }
 
 gpa_status gpa_fp32_attn(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
@@ -470,23 +488,24 @@ gpa_status gpa_fp32_attn(const uint16_t* Q, const uint16_t* K, const uint16_t* V
     if (s != GPA_OK) return s;
     const gpa::Shape sh{(int)(B * H), (int)N, (int)d, causal ? 1 : 0, scale, 1};
     hipStream_t st = (hipStream_t)stream;
-    float* O32 = (float*)workspace;
-    float* Drow = (float*)((char*)workspace + round_up((size_t)B * H * N * d * 4));
+    const F32Layout L = f32_layout(B, H, N, d);
+    char* ws = (char*)workspace;
+    float* O32 = (float*)(ws + L.o32);
+    float* Mrow = (float*)(ws + L.mrow);
+    float* Linv = (float*)(ws + L.linv);
+    float* TS = (float*)(ws + L.ts);
     s = launched(timed(gpa::kKF32Fwd, st,
-                       [&] { return gpa::launch_f32_fwd(Q, K, V, O32, O, LSE, sh, st); }),
+                       [&] { return gpa::launch_f32_fwd(Q, K, V, O32, O, LSE, Mrow, Linv, sh, st); }),
                  "fp32_fwd");
     if (s != GPA_OK) return s;
-    s = launched(timed(gpa::kKF32Pre, st, [&] { return gpa::launch_f32_pre(O32, dO, Drow, sh, st); }),
-                 "fp32_pre");
-    if (s != GPA_OK) return s;
     s = launched(timed(gpa::kKF32Dq, st,
-                       [&] { return gpa::launch_f32_dq(Q, K, V, dO, LSE, Drow, dQ, sh, st); }),
+                       [&] {
+                           return gpa::launch_f32_dq(Q, K, V, dO, O32, Mrow, Linv, TS, dQ, sh, st);
+                       }),
                  "fp32_dq");
     if (s != GPA_OK) return s;
     return launched(timed(gpa::kKF32Dkdv, st,
-                          [&] {
-                              return gpa::launch_f32_dkdv(Q, K, V, dO, LSE, Drow, dK, dV, sh, st);
-                          }),
+                          [&] { return gpa::launch_f32_dkdv(Q, K, V, dO, TS, dK, dV, sh, st); }),
                     "fp32_dkdv");
 }
 
@@ -512,9 +531,8 @@ int gpa_profile_read(double* total_ms, int64_t* launches, int n) {
 }
 
 const char* gpa_kernel_name(int id) {
-    static const char* names[gpa::kNumKernels] = {"fwd_sbs",  "bwd_dq",   "bwd_dkdv",
-                                                  "fp32_fwd", "fp32_pre", "fp32_dq",
-                                                  "fp32_dkdv", "group_sum"};
+    static const char* names[gpa::kNumKernels] = {"fwd_sbs",  "bwd_dq",  "bwd_dkdv", "fp32_fwd",
+                                                  "fp32_dq",  "fp32_dkdv", "group_sum"};
     return (id >= 0 && id < gpa::kNumKernels) ? names[id] : "";
 }
 

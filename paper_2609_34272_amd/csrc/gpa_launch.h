@@ -34,11 +34,10 @@ enum KernelId {
     kKBwdDq = 1,
     kKBwdDkdv = 2,
     kKF32Fwd = 3,
-    kKF32Pre = 4,
-    kKF32Dq = 5,
-    kKF32Dkdv = 6,
-    kKGroupSum = 7,
-    kNumKernels = 8
+    kKF32Dq = 4,
+    kKF32Dkdv = 5,
+    kKGroupSum = 6,
+    kNumKernels = 7
 };
 
 // fma_forward selects the historical exponent rounding (diagnostic only).
@@ -69,16 +68,21 @@ hipError_t launch_bwd_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t*
 hipError_t launch_bwd_group_sum(const float* dKp, const float* dVp, uint16_t* dK, uint16_t* dV,
                                 const Shape& s, hipStream_t st);
 
-// FP32 baseline.
+// Fused FP32 baseline.  The forward writes O (BF16), LSE and, in the
+// workspace, the FP32 output O32 and the scaled row maximum and inverse
+// normaliser per row ([BH, N] each).  The query-major pass forms D =
+// rowsum(dO O32), writes dQ and the per-tile statistics TS ([BH, T, 3, 64]:
+// row maximum, inverse normaliser, D; +inf, 0, 0 beyond N) that the
+// key-major pass stages with each query tile.
 hipError_t launch_f32_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, float* O32,
-                          uint16_t* O, float* LSE, const Shape& s, hipStream_t st);
-hipError_t launch_f32_pre(const float* O32, const uint16_t* dO, float* Drow, const Shape& s,
+                          uint16_t* O, float* LSE, float* Mrow, float* Linv, const Shape& s,
                           hipStream_t st);
 hipError_t launch_f32_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                         const uint16_t* dO, const float* LSE, const float* Drow, uint16_t* dQ,
-                         const Shape& s, hipStream_t st);
+                         const uint16_t* dO, const float* O32, const float* Mrow,
+                         const float* Linv, float* TS, uint16_t* dQ, const Shape& s,
+                         hipStream_t st);
 hipError_t launch_f32_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                           const uint16_t* dO, const float* LSE, const float* Drow,
-                           uint16_t* dK, uint16_t* dV, const Shape& s, hipStream_t st);
+                           const uint16_t* dO, const float* TS, uint16_t* dK, uint16_t* dV,
+                           const Shape& s, hipStream_t st);
 
 }  // namespace gpa
