@@ -27,6 +27,15 @@ sys.path.insert(0, ROOT)
 METRIC = "attn fwd+bwd TFLOP/s at H16 N4096 d64 causal; dQ/dK/dV rel-L2 vs FP64"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
+PEAK_FP32_TFLOPS = 157.3    # MI355X FP32 (vector and matrix)
+
+# Dense contractions per causal (query, key) pair that each kernel forms first
+# (algorithmic), and that it executes (algorithmic + recompute), per mode.
+ALG_PRODUCTS = {"fwd_sbs": {"plain": 2, "gproj_q": 2, "gproj": 2},
+                "bwd_dq": {"plain": 3, "gproj_q": 4, "gproj": 4},        # S, dP, tK (+ rK)
+                "bwd_dkdv": {"plain": 2, "gproj_q": 2, "gproj": 3}}      # r^T dO, t^T Q (+ r^T z)
+EXEC_PRODUCTS = {"fwd_sbs": ALG_PRODUCTS["fwd_sbs"], "bwd_dq": ALG_PRODUCTS["bwd_dq"],
+                 "bwd_dkdv": {m: p + 2 for m, p in ALG_PRODUCTS["bwd_dkdv"].items()}}
 
 
 def parse():
@@ -43,6 +52,10 @@ def parse():
                         "others: tiny, h16_n4096_d128, h16_n16384_d64, b8_h32_n8192_d128)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-accuracy", action="store_true")
+    p.add_argument("--no-configs", action="store_true",
+                   help="skip the timing of the d = 128 and batched workloads")
+    p.add_argument("--no-seeds", action="store_true",
+                   help="skip the 8-seed accuracy protocol of the reference workload")
     p.add_argument("--no-gqa", action="store_true",
                    help="skip the timing of the grouped-query layout (16 query / 4 key-value heads)")
     p.add_argument("--calibrate-copy", action="store_true",
@@ -77,6 +90,112 @@ def recorded_traffic(kernel: str, mode: str, workload: str = "h16_n4096_d64"):
         return None
     k = rec.get("kernels", {}).get(f"{kernel}/{mode}")
     return None if k is None else k.get("hbm_bytes_per_launch")
+
+
+def time_config(gpa, S, wc, seed, iters, dev, to_dev):
+    """Forward and per-mode backward times of one multi-head workload (mean of
+    `iters` calls after ~100 ms of load), its fwd+bwd TFLOP/s by the standard
+    count, the GProj overhead and every kernel's fraction of the bf16 peak by
+    its algorithmic products."""
+    import torch
+    xc = S.make_inputs(wc, seed, workers=16)
+    q, k, v, u = (to_dev(xc[n]) for n in ("q", "k", "v", "do"))
+    del xc
+    B, H, N, d = wc.B, wc.H, wc.N, wc.d
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters
+
+    o, lse = gpa.attn_fwd(q, k, v, wc.causal, wc.scale)
+    # keep the GPU busy for ~100 ms first, so every mode is timed at the same
+    # sustained clock
+    wsw = torch.empty(gpa.attn_bwd_workspace_bytes(B, H, N, d, "gproj"), dtype=torch.uint8,
+                      device=dev)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < 0.1:
+        gpa.attn_bwd(q, k, v, o, lse, u, "gproj", wc.causal, wc.scale, workspace=wsw)
+        torch.cuda.synchronize()
+    del wsw
+    res = {"B": B, "H": H, "N": N, "d": d, "seed": seed, "calls_timed": iters,
+           "fwd_ms": round(timed(lambda: gpa.attn_fwd(q, k, v, wc.causal, wc.scale)), 5),
+           "bwd_ms": {}, "kernel_frac": {}}
+    pairs = B * H * N * N / 2.0
+    for m in gpa.MODES:
+        ws = torch.empty(gpa.attn_bwd_workspace_bytes(B, H, N, d, m), dtype=torch.uint8, device=dev)
+        fn = lambda: gpa.attn_bwd(q, k, v, o, lse, u, m, wc.causal, wc.scale, workspace=ws)  # noqa: E731
+        res["bwd_ms"][m] = round(timed(fn), 5)
+        gpa.profile_enable(True)
+        for _ in range(iters):
+            fn()
+        torch.cuda.synchronize()
+        prof = gpa.profile_read()
+        gpa.profile_enable(False)
+        for name, (tot, cnt) in prof.items():
+            if cnt and name in ALG_PRODUCTS:
+                t = tot / cnt
+                res["kernel_frac"][f"{name}/{m}"] = {
+                    "avg_ms": round(t, 5),
+                    "frac": round(ALG_PRODUCTS[name][m] * 2.0 * d * pairs / (t * 1e-3) / 1e12
+                                  / PEAK_BF16_TFLOPS, 4)}
+        del ws
+    gpa.profile_enable(True)
+    for _ in range(iters):
+        gpa.attn_fwd(q, k, v, wc.causal, wc.scale)
+    torch.cuda.synchronize()
+    prof = gpa.profile_read()
+    gpa.profile_enable(False)
+    tot, cnt = prof["fwd_sbs"]
+    res["kernel_frac"]["fwd_sbs"] = {"avg_ms": round(tot / cnt, 5),
+                                     "frac": round(2 * 2.0 * d * pairs / (tot / cnt * 1e-3) / 1e12
+                                                   / PEAK_BF16_TFLOPS, 4)}
+    flops = 7.0 * d * N * N * B * H
+    res["fwd_bwd_tflops_gproj"] = round(flops / ((res["fwd_ms"] + res["bwd_ms"]["gproj"]) * 1e-3)
+                                        / 1e12, 2)
+    res["gproj_bwd_overhead_vs_plain_pct"] = round(
+        100.0 * (res["bwd_ms"]["gproj"] / res["bwd_ms"]["plain"] - 1), 2)
+    res["gproj_q_bwd_overhead_vs_plain_pct"] = round(
+        100.0 * (res["bwd_ms"]["gproj_q"] / res["bwd_ms"]["plain"] - 1), 2)
+    del q, k, v, u, o, lse
+    torch.cuda.empty_cache()
+    return res
+
+
+def seed_protocol(gpa, S, oracle, w, index, to_dev):
+    """Accuracy over the eight seeds 1000*index + s (s = 0..7) of a workload:
+    per-seed and median full-tensor relative L2 (%) against the FP64 oracle
+    for O, dQ, dK, dV in every mode and for the FP32 baseline (the paper
+    reports medians over its eight captures)."""
+    import numpy as np
+    import torch
+    seeds = S.seeds_for(index, 8)
+    names = ("O", "dQ", "dK", "dV")
+    per = {m: {n: [] for n in names} for m in (*gpa.MODES, "fp32")}
+    for seed in seeds:
+        x = S.make_inputs(w, seed, workers=16)
+        q, k, v, u = (to_dev(x[n]) for n in ("q", "k", "v", "do"))
+        o, lse = gpa.attn_fwd(q, k, v, w.causal, w.scale)
+        res = {m: (o, *gpa.attn_bwd(q, k, v, o, lse, u, m, w.causal, w.scale)) for m in gpa.MODES}
+        fo, _, fdq, fdk, fdv = gpa.fp32_attn(q, k, v, u, w.causal, w.scale)
+        res["fp32"] = (fo, fdq, fdk, fdv)
+        torch.cuda.synchronize()
+        ex = oracle.exact(x["q"], x["k"], x["v"], x["do"], w.causal, w.scale)
+        for m, ts in res.items():
+            for n, t in zip(names, ts):
+                per[m][n].append(round(oracle.rel_l2(
+                    t.float().cpu().numpy().astype(np.float64), ex[n]), 4))
+    return {"workload": w.name, "seeds": seeds, "per_seed": per,
+            "median": {m: {n: round(float(np.median(vals)), 4) for n, vals in d_.items()}
+                       for m, d_ in per.items()}}
 
 
 def main():
@@ -153,6 +272,10 @@ def main():
         bwd_ms[m] = timed(lambda: gpa.attn_bwd(q, k, v, o, lse, u, m, w.causal, w.scale,
                                                workspace=ws[m]), args.steps)
     fwd_ms = timed(lambda: gpa.attn_fwd(q, k, v, w.causal, w.scale), args.steps)
+    # The same K steps timed again, now that the sections above have kept the
+    # GPU busy: the part raises its clock over the first tens of milliseconds
+    # of load, so with few warmup steps `ms_per_step` includes that ramp.
+    ms_again = timed(lambda: step(args.mode), args.steps)
 
     # Per-call distribution (p10 / median / p90 ms): each call bracketed by its
     # own pair of events, so each figure carries a few microseconds of event
@@ -200,28 +323,62 @@ def main():
             100.0 * (gqa["bwd_ms"]["gproj"] / gqa["bwd_ms"]["plain"] - 1), 2)
         del qg, kg, vg, ug, og, lg
 
-    # The FP32-arithmetic attention (forward + backward in one call, BF16 I/O):
-    # the accuracy-class baseline, timed beside the BF16 path (last: its long
-    # vector-ALU load lowers the clock for what follows).
+    # The fused FP32 attention (forward + backward in one call, BF16 I/O, FP32
+    # products and accumulation on the FP32 matrix cores): the accuracy-class
+    # baseline, timed beside the BF16 path, with its own fraction of the FP32
+    # peak by the standard count and per kernel.
     for _ in range(2):
         gpa.fp32_attn(q, k, v, u, w.causal, w.scale)
     fp32_ms = timed(lambda: gpa.fp32_attn(q, k, v, u, w.causal, w.scale), max(5, args.steps // 5))
+    gpa.profile_enable(True)
+    for _ in range(max(5, args.steps // 5)):
+        gpa.fp32_attn(q, k, v, u, w.causal, w.scale)
+    torch.cuda.synchronize()
+    fprof = gpa.profile_read()
+    gpa.profile_enable(False)
+    fp32_kern = {n: round(t / c, 5) for n, (t, c) in fprof.items() if c and n.startswith("fp32")}
+    fp32 = {"fwd_bwd_ms": round(fp32_ms, 5),
+            "tflops_standard_count": round(flops / (fp32_ms * 1e-3) / 1e12, 2),
+            "frac_of_fp32_peak": round(flops / (fp32_ms * 1e-3) / 1e12 / PEAK_FP32_TFLOPS, 4),
+            "peak": PEAK_FP32_TFLOPS, "kernels_ms": fp32_kern,
+            # products per causal pair each kernel executes (fwd QK^T, PV; query
+            # pass QK^T, dO V^T, dS K; key pass QK^T, dO V^T, P^T dO, dS^T Q)
+            "kernel_frac_executed": {
+                n: round(p * 2.0 * d * B * H * N * N / 2.0 / (fp32_kern[n] * 1e-3) / 1e12
+                         / PEAK_FP32_TFLOPS, 4)
+                for n, p in (("fp32_fwd", 2), ("fp32_dq", 3), ("fp32_dkdv", 4)) if n in fp32_kern}}
 
-    # Roofline of the dominant kernel: algorithmic MFMA flops per launch.
+    # Roofline of the dominant kernel.  Algorithmic flops count each dense
+    # contraction of the method once over the whole path (forward: QK^T, PV;
+    # backward: QK^T, dO V^T, tK, r^T dO, t^T Q, and for GProj rK and r^T z):
+    # a kernel is credited only with the products it forms first.  The key pass
+    # recomputes S = QK^T and dP = dO V^T, which the query pass already formed
+    # (schedule-dependent recompute, reported separately as executed products).
     pairs = B * H * N * N / 2.0
-    # dense contractions each kernel needs for its own outputs (per causal pair, 2d flops each):
-    # fwd: QK^T, PV; bwd_dq: QK^T, dO V^T, tK (+ rK); bwd_dkdv: QK^T, dO V^T, r^T dO, t^T Q (+ r^T z)
-    gp = args.mode != "plain"
-    gemms = {"fwd_sbs": 2, "bwd_dq": 4 if gp else 3, "bwd_dkdv": 5 if args.mode == "gproj" else 4}
-    dom = max((n for n in kern if n in gemms), key=lambda n: kern[n])
-    alg = gemms[dom] * 2.0 * d * pairs
+    flop_pair = 2.0 * d  # one dense contraction per causal (query, key) pair
+    dom = max((n for n in kern if n in ALG_PRODUCTS), key=lambda n: kern[n])
+    alg_p = ALG_PRODUCTS[dom][args.mode]
+    exe_p = EXEC_PRODUCTS[dom][args.mode]
+    alg = alg_p * flop_pair * pairs
     achieved = alg / (kern[dom] * 1e-3) / 1e12
+    bwd_kern_ms = sum(kern[n] for n in ("bwd_dq", "bwd_dkdv") if n in kern)
+    bwd_alg_products = {"plain": 5, "gproj_q": 6, "gproj": 7}[args.mode]
     roofline = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                 "traffic": recorded_traffic(dom, args.mode, w.name),
                 "avg_ms": round(kern[dom], 5),
-                "algorithmic_flops_per_launch": alg}
+                "algorithmic_products_per_pair": alg_p,
+                "algorithmic_flops_per_launch": alg,
+                "executed_products_per_pair": exe_p,
+                "executed_frac": round(exe_p * flop_pair * pairs / (kern[dom] * 1e-3) / 1e12
+                                       / PEAK_BF16_TFLOPS, 4),
+                # the whole backward of this mode (both passes) by the method's
+                # algorithmic count: plain 5, gproj_q 6, gproj 7 products per pair
+                "backward_algorithmic_products_per_pair": bwd_alg_products,
+                "backward_kernels_ms": round(bwd_kern_ms, 5),
+                "backward_frac": round(bwd_alg_products * flop_pair * pairs / (bwd_kern_ms * 1e-3)
+                                       / 1e12 / PEAK_BF16_TFLOPS, 4)}
 
     out = {
         "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
@@ -238,12 +395,23 @@ def main():
         "per_call_ms_p10_p50_p90": per_call,
         "gproj_bwd_overhead_vs_plain_pct": round(100.0 * (bwd_ms["gproj"] / bwd_ms["plain"] - 1), 2),
         "gproj_q_bwd_overhead_vs_plain_pct": round(100.0 * (bwd_ms["gproj_q"] / bwd_ms["plain"] - 1), 2),
-        "fp32_attn_fwd_bwd_ms": round(fp32_ms, 5),
+        "fp32_attn": fp32,
         "fp32_attn_vs_gproj_fwd_bwd": round(fp32_ms / (fwd_ms + bwd_ms["gproj"]), 3),
         "wall_s_timed": round(wall, 3),
+        "ms_per_step_retimed_after_load": round(ms_again, 5),
     }
     if gqa is not None:
         out["gqa"] = gqa
+
+    # The wider-head and batched workloads, timed on the same kernels (their
+    # parity is covered by the tests): forward and backward per mode, the GProj
+    # overhead and each kernel's fraction of the bf16 peak by its algorithmic
+    # products.
+    if not args.no_configs and w.name == "h16_n4096_d64":
+        out["configs"] = {}
+        for idx, iters in ((3, 50), (5, 6)):
+            wc = S.WORKLOADS[idx]
+            out["configs"][wc.name] = time_config(gpa, S, wc, 1000 * idx, iters, dev, to_dev)
 
     if not args.no_accuracy or not args.no_cpu_baseline:
         import oracle
@@ -283,6 +451,8 @@ def main():
                 acc[m] = {n: round(oracle.rel_l2(host(t), ex[n]), 4)
                           for n, t in (("O", oo), ("dQ", dq), ("dK", dk), ("dV", dv))}
             out["rel_l2_pct_vs_fp64"] = acc
+            if not args.no_seeds and nh == B * H:
+                out["seed_protocol"] = seed_protocol(gpa, S, oracle, w, wid[w.name], to_dev)
             # Context: the regime of the paper's captures (near one-hot rows at
             # a logit scale of ~10^4, large common key offset), where the
             # forward's exponent rounding matters: FA3 (FMA forward + plain),

@@ -124,13 +124,15 @@ def make_head(w: Workload, seed: int, b: int, h: int, N: int | None = None):
     return _to_bf16(q), _to_bf16(k), _to_bf16(v0), _to_bf16(u)
 
 
-def make_inputs(w: Workload, seed: int, heads=None):
+def make_inputs(w: Workload, seed: int, heads=None, workers: int = 1):
     """Generate a workload as uint16 BF16 bit arrays: q, do [B, H, N, d] and
     k, v [B, Hkv, N, d].
 
     heads: optional list of (b, h) pairs (multi-head workloads only); if given,
     the arrays are shaped [len(heads), 1, N, d] holding only those heads (same
     values as in the full tensor).
+    workers: threads drawing heads concurrently (every head has its own
+    generator, so the values do not depend on it).
     """
     Hkv = w.kv_heads
     if heads is not None and Hkv != w.H:
@@ -145,7 +147,9 @@ def make_inputs(w: Workload, seed: int, heads=None):
     G = w.H // Hkv
     out = {n: np.empty(shape, dtype=np.uint16) for n in ("q", "do")}
     out.update({n: np.empty(kv_shape, dtype=np.uint16) for n in ("k", "v")})
-    for idx, (b, h) in enumerate(pairs):
+
+    def one(idx):
+        b, h = pairs[idx]
         q, k, v, u = make_head(w, seed, b, h)
         bi, hi = divmod(idx, shape[1])
         out["q"][bi, hi] = q
@@ -156,4 +160,12 @@ def make_inputs(w: Workload, seed: int, heads=None):
         elif hi % G == 0:
             out["k"][bi, hi // G] = k
             out["v"][bi, hi // G] = v
+
+    if workers > 1 and len(pairs) > 1:
+        from concurrent.futures import ThreadPoolExecutor
+        with ThreadPoolExecutor(max_workers=workers) as ex:
+            list(ex.map(one, range(len(pairs))))
+    else:
+        for idx in range(len(pairs)):
+            one(idx)
     return out
