@@ -126,6 +126,33 @@ gpa_status gpa_attn_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Backward without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation).  Same arguments, arithmetic and results as
+ * gpa_attn_bwd (multi-head only) -- bitwise the same outputs -- but its
+ * scratch (the row statistics, the per-tile statistics and z, exactly what
+ * gpa_attn_bwd keeps in its workspace) lives in the library's own static
+ * device array of gpa_attn_bwd_noalloc_max_bytes() bytes (64 MiB), one per
+ * GPU, held until the process ends.  The array of the current device is
+ * used: the stream must belong to it.  No call allocates or frees memory;
+ * the first call on a device looks up the array's address there
+ * (hipGetSymbolAddress).  Nothing in the scratch needs to start at any
+ * value: every call writes what it reads.  Every call on one GPU shares the
+ * array, so calls that overlap in time on one GPU (concurrent streams,
+ * threads) race and give wrong results; serialise them.
+ * Errors as gpa_attn_bwd, and GPA_EWORKSPACE (nothing launched) when the
+ * shape needs more scratch than the array holds, i.e. when
+ * gpa_attn_bwd_workspace_bytes(B, H, N, d, mode) > gpa_attn_bwd_noalloc_max_bytes()
+ * (e.g. B*H*N above about 430 000 rows at d = 64 in gproj mode).
+ */
+size_t gpa_attn_bwd_noalloc_max_bytes(void);
+gpa_status gpa_attn_bwd_noalloc(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                                const uint16_t* O, const float* LSE, const uint16_t* dO,
+                                uint16_t* dQ, uint16_t* dK, uint16_t* dV,
+                                int64_t B, int64_t H, int64_t N, int64_t d,
+                                int causal, float scale, int mode, void* stream);
+
+/*
  * Byte offsets, inside the backward workspace, of the FP32 [B,H,N] arrays D
  * (preprocess row statistic), rho (row mass of t), m (row mass of r) and
  * lambda = rho/m (Algorithm 1; eq. gproj-row-mass).  Any pointer may be NULL.

@@ -31,7 +31,7 @@ __all__ = [
     "MODES", "lib", "attn_fwd", "attn_fwd_fma", "attn_bwd", "attn_bwd_workspace_bytes", "bwd_stats_offsets",
     "attn_fwd_varlen", "attn_bwd_varlen", "attn_bwd_varlen_workspace_bytes",
     "fp32_attn", "fp32_attn_workspace_bytes", "profile_enable", "profile_read", "GpaError",
-    "LIB_PATH", "attention", "attention_varlen",
+    "LIB_PATH", "attention", "attention_varlen", "attn_bwd_noalloc",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -92,6 +92,11 @@ def lib():
     L.gpa_fp32_attn.argtypes = [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, INT, F32, P, SZ, P]
     L.gpa_profile_enable.restype = None
     L.gpa_profile_enable.argtypes = [INT]
+    L.gpa_attn_bwd_noalloc_max_bytes.restype = SZ
+    L.gpa_attn_bwd_noalloc_max_bytes.argtypes = []
+    L.gpa_attn_bwd_noalloc.restype = INT
+    L.gpa_attn_bwd_noalloc.argtypes = [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, INT, F32,
+                                       INT, P]
     L.gpa_profile_read.restype = INT
     L.gpa_profile_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64), INT]
     L.gpa_kernel_name.restype = ctypes.c_char_p
@@ -230,6 +235,30 @@ def attn_bwd(q, k, v, o, lse, do, mode: str = "gproj", causal: bool = True, scal
     stats = {name: workspace[off:off + 4 * n].view(torch.float32).view(B, H, N)
              for name, off in offs.items()}
     return dq, dk, dv, stats
+
+
+def attn_bwd_noalloc(q, k, v, o, lse, do, mode: str = "gproj", causal: bool = True, scale=None,
+                     out=None):
+    """attn_bwd without a workspace: the library uses its own per-GPU scratch
+    array (gpa_attn_bwd_noalloc; multi-head only, shapes whose workspace fits
+    gpa_attn_bwd_noalloc_max_bytes()).  out: optional preallocated (dq, dk,
+    dv); otherwise they are allocated here.  Calls that overlap on one GPU
+    share the scratch and race."""
+    B, H, N, d = _shape(q)
+    for t, n in ((q, "q"), (k, "k"), (v, "v"), (o, "o"), (do, "do")):
+        _need(t, n, (B, H, N, d), torch.bfloat16)
+    _need(lse, "lse", (B, H, N), torch.float32)
+    mcode = MODES[mode] if isinstance(mode, str) else int(mode)
+    if out is None:
+        out = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v))
+    dq, dk, dv = out
+    for t, n in ((dq, "dq"), (dk, "dk"), (dv, "dv")):
+        _need(t, n, (B, H, N, d), torch.bfloat16)
+    _check(lib().gpa_attn_bwd_noalloc(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                      lse.data_ptr(), do.data_ptr(), dq.data_ptr(), dk.data_ptr(),
+                                      dv.data_ptr(), B, H, N, d, int(bool(causal)),
+                                      _scale(d, scale), mcode, _stream(q)))
+    return dq, dk, dv
 
 
 def _offsets(cu, name):

@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -252,6 +253,40 @@ gpa::Shape varlen_shape(const Varlen& v, int causal, float scale) {
     return sh;
 }
 
+// ------------------------------------------------- no-allocation scratch
+// Device memory of gpa_attn_bwd_noalloc: the backward's workspace (row
+// statistics, per-tile statistics, z) for callers that cannot allocate.  One
+// copy per GPU, held until the process ends; every call on a GPU shares it.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+// Host code never passes `scratch` itself to a kernel: on the host the name
+// is a stand-in, not a device address.  Its address on each device comes
+// from hipGetSymbolAddress, taken once per device with that device current.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+gpa_status scratch_address(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(GPA_EHIP, "hipGetDevice failed: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(GPA_EHIP, "device %d beyond the %d devices the scratch table covers", dev,
+                    kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(GPA_EHIP, "hipGetSymbolAddress(scratch) on device %d failed: %s", dev,
+                        hipGetErrorString(e));
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return GPA_OK;
+}
+
 BwdLayout varlen_layout(const Varlen& v, int mode) {
     return bwd_layout_rows((size_t)v.Hq * v.total_q, (size_t)v.Hq * v.total_k,
                            (size_t)v.nseq * v.Hq, v.max_q, v.d, mode, v.Hq > v.Hkv);
@@ -391,6 +426,34 @@ gpa_status gpa_attn_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                             workspace, workspace_bytes, stream);
 }
 
+
+size_t gpa_attn_bwd_noalloc_max_bytes(void) { return kScratchBytes; }
+
+gpa_status gpa_attn_bwd_noalloc(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                                const uint16_t* O, const float* LSE, const uint16_t* dO,
+                                uint16_t* dQ, uint16_t* dK, uint16_t* dV, int64_t B, int64_t H,
+                                int64_t N, int64_t d, int causal, float scale, int mode,
+                                void* stream) {
+    gpa_status s = check_shape(B, H, N, d, scale);
+    if (s != GPA_OK) return s;
+    if (mode < 0 || mode > 2) return fail(GPA_EINVAL, "mode %d is not 0, 1 or 2", mode);
+    const size_t need = gpa_attn_bwd_workspace_bytes(B, H, N, d, mode);
+    if (need > kScratchBytes)
+        return fail(GPA_EWORKSPACE,
+                    "this shape needs %zu bytes of scratch; gpa_attn_bwd_noalloc holds at most %zu "
+                    "(use gpa_attn_bwd with a workspace)",
+                    need, kScratchBytes);
+    const size_t tb = (size_t)B * H * N * d * 2, lb = (size_t)B * H * N * 4;
+    s = check_ptrs({{Q, tb, "Q"}, {K, tb, "K"}, {V, tb, "V"}, {O, tb, "O"}, {LSE, lb, "LSE"},
+                    {dO, tb, "dO"}},
+                   {{dQ, tb, "dQ"}, {dK, tb, "dK"}, {dV, tb, "dV"}});
+    if (s != GPA_OK) return s;
+    void* ws = nullptr;
+    if ((s = scratch_address(&ws)) != GPA_OK) return s;
+    const gpa::Shape sh{(int)(B * H), (int)N, (int)d, causal ? 1 : 0, scale, 1};
+    return run_bwd(Q, K, V, O, LSE, dO, dQ, dK, dV, sh, bwd_layout(B, H, H, N, d, mode),
+                   (size_t)B * H * N, mode, ws, (hipStream_t)stream);
+}
 
 gpa_status gpa_attn_fwd_varlen(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                                uint16_t* O, float* LSE, const int32_t* cu_seqlens_q,
