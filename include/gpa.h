@@ -153,6 +153,28 @@ gpa_status gpa_attn_bwd_noalloc(const uint16_t* Q, const uint16_t* K, const uint
                                 int causal, float scale, int mode, void* stream);
 
 /*
+ * Plain backward as one key-major pass with FP32 atomic dQ (Algorithm 1's
+ * first loop without the GProj additions: dQ accumulated by atomic adds while
+ * dK and dV stay with their key tile), for measurement beside the two-pass
+ * schedule gpa_attn_bwd uses.  Dense multi-head only; arguments as
+ * gpa_attn_bwd in plain mode.  Three kernels: D and the per-tile statistics
+ * (bitwise those of gpa_attn_bwd's query-major pass) with the FP32 dQ
+ * accumulator zeroed; the key-major pass, whose dK and dV are bitwise those of
+ * gpa_attn_bwd in plain mode and which adds each tile's t K into the
+ * accumulator with device-scope FP32 atomics; dQ = BF16(fl32(scale A)).  The
+ * atomic order varies between runs, so dQ is not bitwise reproducible (its
+ * FP32 sums are the same terms in another order).  workspace: at least
+ * gpa_attn_bwd_atomic_workspace_bytes(...) bytes, 256-byte aligned.
+ */
+size_t gpa_attn_bwd_atomic_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d);
+gpa_status gpa_attn_bwd_atomic(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                               const uint16_t* O, const float* LSE, const uint16_t* dO,
+                               uint16_t* dQ, uint16_t* dK, uint16_t* dV,
+                               int64_t B, int64_t H, int64_t N, int64_t d,
+                               int causal, float scale,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Byte offsets, inside the backward workspace, of the FP32 [B,H,N] arrays D
  * (preprocess row statistic), rho (row mass of t), m (row mass of r) and
  * lambda = rho/m (Algorithm 1; eq. gproj-row-mass).  Any pointer may be NULL.

@@ -31,7 +31,8 @@ __all__ = [
     "MODES", "lib", "attn_fwd", "attn_fwd_fma", "attn_bwd", "attn_bwd_workspace_bytes", "bwd_stats_offsets",
     "attn_fwd_varlen", "attn_bwd_varlen", "attn_bwd_varlen_workspace_bytes",
     "fp32_attn", "fp32_attn_workspace_bytes", "profile_enable", "profile_read", "GpaError",
-    "LIB_PATH", "attention", "attention_varlen", "attn_bwd_noalloc",
+    "LIB_PATH", "attention", "attention_varlen", "attn_bwd_noalloc", "attn_bwd_atomic",
+    "attn_bwd_atomic_workspace_bytes",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -97,6 +98,11 @@ def lib():
     L.gpa_attn_bwd_noalloc.restype = INT
     L.gpa_attn_bwd_noalloc.argtypes = [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, INT, F32,
                                        INT, P]
+    L.gpa_attn_bwd_atomic_workspace_bytes.restype = SZ
+    L.gpa_attn_bwd_atomic_workspace_bytes.argtypes = [I64, I64, I64, I64]
+    L.gpa_attn_bwd_atomic.restype = INT
+    L.gpa_attn_bwd_atomic.argtypes = [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, INT, F32, P,
+                                      SZ, P]
     L.gpa_profile_read.restype = INT
     L.gpa_profile_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64), INT]
     L.gpa_kernel_name.restype = ctypes.c_char_p
@@ -235,6 +241,29 @@ def attn_bwd(q, k, v, o, lse, do, mode: str = "gproj", causal: bool = True, scal
     stats = {name: workspace[off:off + 4 * n].view(torch.float32).view(B, H, N)
              for name, off in offs.items()}
     return dq, dk, dv, stats
+
+
+def attn_bwd_atomic(q, k, v, o, lse, do, causal: bool = True, scale=None, workspace=None):
+    """Plain backward as one key-major pass with FP32 atomic dQ
+    (gpa_attn_bwd_atomic; dense multi-head).  dK, dV bitwise those of
+    attn_bwd(mode="plain"); dQ the same sums in another order."""
+    B, H, N, d = _shape(q)
+    for t, n in ((q, "q"), (k, "k"), (v, "v"), (o, "o"), (do, "do")):
+        _need(t, n, (B, H, N, d), torch.bfloat16)
+    _need(lse, "lse", (B, H, N), torch.float32)
+    nbytes = int(lib().gpa_attn_bwd_atomic_workspace_bytes(B, H, N, d))
+    if workspace is None:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    _check(lib().gpa_attn_bwd_atomic(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                     lse.data_ptr(), do.data_ptr(), dq.data_ptr(), dk.data_ptr(),
+                                     dv.data_ptr(), B, H, N, d, int(bool(causal)), _scale(d, scale),
+                                     workspace.data_ptr(), workspace.numel(), _stream(q)))
+    return dq, dk, dv
+
+
+def attn_bwd_atomic_workspace_bytes(B: int, H: int, N: int, d: int) -> int:
+    return int(lib().gpa_attn_bwd_atomic_workspace_bytes(B, H, N, d))
 
 
 def attn_bwd_noalloc(q, k, v, o, lse, do, mode: str = "gproj", causal: bool = True, scale=None,

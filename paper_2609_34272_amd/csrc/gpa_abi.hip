@@ -455,6 +455,52 @@ gpa_status gpa_attn_bwd_noalloc(const uint16_t* Q, const uint16_t* K, const uint
                    (size_t)B * H * N, mode, ws, (hipStream_t)stream);
 }
 
+size_t gpa_attn_bwd_atomic_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d) {
+    if (B < 1 || H < 1 || N < 1 || (d != 64 && d != 128)) return 0;
+    if ((double)B * H * N * d >= 2147483648.0) return 0;
+    const size_t T = (size_t)(N + 63) / 64;
+    return round_up((size_t)B * H * T * 128 * sizeof(float)) +
+           round_up((size_t)B * H * N * d * sizeof(float));
+}
+
+gpa_status gpa_attn_bwd_atomic(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                               const uint16_t* O, const float* LSE, const uint16_t* dO,
+                               uint16_t* dQ, uint16_t* dK, uint16_t* dV, int64_t B, int64_t H,
+                               int64_t N, int64_t d, int causal, float scale, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+    gpa_status s = check_shape(B, H, N, d, scale);
+    if (s != GPA_OK) return s;
+    const size_t need = gpa_attn_bwd_atomic_workspace_bytes(B, H, N, d);
+    if (!workspace || workspace_bytes < need)
+        return fail(GPA_EWORKSPACE, "workspace %p of %zu bytes; %zu needed", workspace,
+                    workspace_bytes, need);
+    if ((uintptr_t)workspace % kAlign)
+        return fail(GPA_EWORKSPACE, "workspace is not %zu-byte aligned", kAlign);
+    const size_t tb = (size_t)B * H * N * d * 2, lb = (size_t)B * H * N * 4;
+    s = check_ptrs({{Q, tb, "Q"}, {K, tb, "K"}, {V, tb, "V"}, {O, tb, "O"}, {LSE, lb, "LSE"},
+                    {dO, tb, "dO"}},
+                   {{dQ, tb, "dQ"}, {dK, tb, "dK"}, {dV, tb, "dV"}, {workspace, need, "workspace"}});
+    if (s != GPA_OK) return s;
+    const gpa::Shape sh{(int)(B * H), (int)N, (int)d, causal ? 1 : 0, scale, 1};
+    hipStream_t st = (hipStream_t)stream;
+    const size_t T = (size_t)(N + 63) / 64;
+    float* TS = (float*)workspace;
+    float* acc = (float*)((char*)workspace + round_up((size_t)B * H * T * 128 * sizeof(float)));
+    s = launched(timed(gpa::kKBwdPre, st,
+                       [&] { return gpa::launch_bwd_pre(O, dO, LSE, TS, acc, sh, st); }),
+                 "bwd_pre");
+    if (s != GPA_OK) return s;
+    s = launched(timed(gpa::kKBwdFused, st,
+                       [&] {
+                           return gpa::launch_bwd_fused_plain(Q, K, V, dO, TS, dK, dV, acc, sh, st);
+                       }),
+                 "bwd_fused_plain");
+    if (s != GPA_OK) return s;
+    return launched(timed(gpa::kKBwdFinal, st,
+                          [&] { return gpa::launch_bwd_dq_finalize(acc, dQ, sh, st); }),
+                    "bwd_dq_finalize");
+}
+
 gpa_status gpa_attn_fwd_varlen(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                                uint16_t* O, float* LSE, const int32_t* cu_seqlens_q,
                                const int32_t* cu_seqlens_k, int64_t nseq, int64_t total_q,
@@ -594,8 +640,9 @@ int gpa_profile_read(double* total_ms, int64_t* launches, int n) {
 }
 
 const char* gpa_kernel_name(int id) {
-    static const char* names[gpa::kNumKernels] = {"fwd_sbs",  "bwd_dq",  "bwd_dkdv", "fp32_fwd",
-                                                  "fp32_dq",  "fp32_dkdv", "group_sum"};
+    static const char* names[gpa::kNumKernels] = {
+        "fwd_sbs",   "bwd_dq",  "bwd_dkdv",        "fp32_fwd",       "fp32_dq",
+        "fp32_dkdv", "group_sum", "bwd_pre", "bwd_fused_plain", "bwd_dq_finalize"};
     return (id >= 0 && id < gpa::kNumKernels) ? names[id] : "";
 }
 

@@ -410,14 +410,21 @@ __device__ __forceinline__ void dkdv_probs(const f32x4& s, const f32x4& dp, cons
     }
 }
 
-template <int D, bool GPROJ>
+// FUSED_DQ (plain mode, dense multi-head only): the single key-major pass of
+// Algorithm 1's first loop without the GProj additions.  Besides dV and dK it
+// forms this key tile's share of A = tK for every query tile it visits and
+// adds it into the FP32 accumulator dQacc [BH, N, d] with device-scope atomic
+// adds (dQ = BF16(alpha A) is formed afterwards).  t goes through LDS once per
+// step, as the transposed operand of that product.
+template <int D, bool GPROJ, bool FUSED_DQ = false>
 __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dkdv_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, const uint16_t* __restrict__ dO,
     const float* __restrict__ TS, const uint16_t* __restrict__ Z, uint16_t* __restrict__ dK,
     uint16_t* __restrict__ dV, float* __restrict__ dKp, float* __restrict__ dVp, int BH, int Nmax,
     int causal, float scale, int G, const int* __restrict__ cu, int Hq, int total,
-    const int* __restrict__ cu_k, int total_k, int Nkmax) {
+    const int* __restrict__ cu_k, int total_k, int Nkmax, float* __restrict__ dQacc = nullptr) {
+    static_assert(!(FUSED_DQ && GPROJ), "the fused pass is the plain backward");
     constexpr int MB = D / 16;
     constexpr int KC = D / 32;
     constexpr int NT = GPROJ ? 3 : 2;  // staged tensors: Q, dO (and Z = BF16(lambda Q))
@@ -434,6 +441,9 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     __shared__ __attribute__((aligned(16))) uint16_t B0[SLOT_E];
     __shared__ __attribute__((aligned(16))) uint16_t B1[SLOT_E];
     __shared__ __attribute__((aligned(16))) uint16_t B2[SLOT_E];
+    // fused dQ: this tile's keys [key][d] and the step's t as [key][query]
+    __shared__ __attribute__((aligned(16))) uint16_t Ks[FUSED_DQ ? TILE_E : 8];
+    __shared__ __attribute__((aligned(16))) uint16_t Xt[FUSED_DQ ? kTile * kTile : 8];
 
     const int Tq = (Nmax + kTile - 1) / kTile;   // query tiles of the longest problem
     const int Tk = (Nkmax + kTile - 1) / kTile;  // key tiles of the longest problem
@@ -522,6 +532,12 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     // compiler cannot count the fills, so it must have nothing left to wait
     // for inside the loop.
     wait_vm_lgkm0<0>();
+    if constexpr (FUSED_DQ) {
+        dma.load(K + kvoff, Ks, tile * kTile, Nk);
+        wait_vm_lgkm0<0>();
+    }
+    const rsrc_t rdq = make_rsrc(FUSED_DQ ? dQacc + hoff : nullptr,
+                                 FUSED_DQ ? (uint32_t)N * (uint32_t)D * 4u : 0u);
     fill(B0, qt0);
     fill(B1, qt0 + 1);
     wait_vm_lgkm0<FILL_VM>();
@@ -611,8 +627,54 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
             if (mb + 2 < MB) read_ops(opd[mb & 1], mb + 2);
             fill_piece(nxt2, qt + 2, AT_START + 4 + mb);
         }
-        // Tile qt + 1 must have landed; tile qt + 2 may stay in flight.
-        wait_vm_lgkm0<FILL_VM>();
+        if constexpr (FUSED_DQ) {
+            // t of this wave's 32 keys x 32 queries into Xt[key][query]: lane
+            // (c16, g) holds key 32 kh + 16 kb + c16 at queries 32 qh + 16 mq +
+            // 4 g + i, i.e. 8 contiguous bytes of one Xt row per (kb, mq).
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int mq = 0; mq < 2; ++mq) {
+                    bf16x4 w4;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) w4[i] = tf[kb][4 * mq + i];
+                    *reinterpret_cast<bf16x4*>(
+                        Xt + tile_off<kTile>(32 * kh + 16 * kb + c16, 32 * qh + 16 * mq + 4 * g)) = w4;
+                }
+            __syncthreads();
+            // A block of this tile's share of A = tK: wave w takes queries
+            // 16 w .. 16 w + 15 against all 64 keys.  Operands: t[query][key]
+            // and K[key][d], both read transposed (key along k).
+            f32x4 aq[MB];
+#pragma unroll
+            for (int db = 0; db < MB; ++db) aq[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kc = 0; kc < 2; ++kc) {
+                const bf16x8 ta = ld_tr_operand<kTile>(Xt, 32 * kc, 16 * wave, c16, g);
+#pragma unroll
+                for (int db = 0; db < MB; ++db)
+                    aq[db] = mfma_16x16x32(ta, ld_tr_operand<D>(Ks, 32 * kc, 16 * db, c16, g), aq[db]);
+            }
+            // FP32 atomic adds through a buffer resource over this head's N
+            // rows (rows beyond N are dropped by the range check): lanes c16
+            // cover 16 consecutive columns of one query row, 64 contiguous
+            // bytes per row and instruction.
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t off = (uint32_t)((q0 + 16 * wave + 4 * g + i) * D + c16) * 4u;
+#pragma unroll
+                for (int db = 0; db < MB; ++db)
+                    __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(aq[db][i], rdq, off + 64u * db, 0,
+                                                                    0);
+            }
+            // The atomics share the vector-memory counter with the tile
+            // fills; wait for everything rather than rely on the order in
+            // which writes and loads complete.
+            wait_vm_lgkm0<0>();
+        } else {
+            // Tile qt + 1 must have landed; tile qt + 2 may stay in flight.
+            wait_vm_lgkm0<FILL_VM>();
+        }
         __builtin_amdgcn_s_barrier();
     };
     const std::false_type plain;
@@ -725,7 +787,105 @@ __global__ __launch_bounds__(256) void group_sum_kernel(const float* __restrict_
     st_bf16x4(dV + kvh * per_head + e, sv[0], sv[1], sv[2], sv[3]);
 }
 
+// Preprocessing of the fused plain pass (dense multi-head): Algorithm 1's
+// D_i = sum_c fl32(dO_ic O_ic) with the query-major pass's own lanes and
+// summation order (so its bits, and hence t, equal that pass's), the per-tile
+// statistics block the key-major pass stages, and a zeroed dQ accumulator.
+// One workgroup per (head, 64-row tile); wave w takes rows 16 w .. 16 w + 15.
+template <int D>
+__global__ __launch_bounds__(kThreads) void bwd_pre_kernel(const uint16_t* __restrict__ O,
+                                                           const uint16_t* __restrict__ dO,
+                                                           const float* __restrict__ LSE,
+                                                           float* __restrict__ TS,
+                                                           float* __restrict__ dQacc, int BH,
+                                                           int N) {
+    constexpr int KC = D / 32;
+    const int T = (N + kTile - 1) / kTile;
+    const int bh = blockIdx.x / T, tile = blockIdx.x - bh * T;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int g = lane >> 4, c16 = lane & 15;
+    const int qrow = tile * kTile + 16 * wave + c16;
+    const size_t hoff = (size_t)bh * N * D;
+    const uint32_t tb = (uint32_t)N * (2 * D);
+    const rsrc_t ru = make_rsrc(dO + hoff, tb);
+    const rsrc_t ro = make_rsrc(O + hoff, tb);
+    float dpart = 0.f;
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc) {
+        const u32x4 uw = ld_row16<D>(ru, qrow, kc * 32 + 8 * g);
+        const u32x4 ow = ld_row16<D>(ro, qrow, kc * 32 + 8 * g);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            dpart += lo_bf16(uw[e]) * lo_bf16(ow[e]);
+            dpart += hi_bf16(uw[e]) * hi_bf16(ow[e]);
+        }
+    }
+    const float Di = xor_sum(dpart);
+    if (g == 0) {
+        float* ts = TS + ((size_t)bh * T + tile) * kStatFloats;
+        ts[16 * wave + c16] = qrow < N ? LSE[(size_t)bh * N + qrow] * kLog2e : INFINITY;
+        ts[kTile + 16 * wave + c16] = Di;
+    }
+    if (qrow < N) {
+        float* a = dQacc + hoff + (size_t)qrow * D;
+#pragma unroll
+        for (int c = 0; c < D / 4; c += 4)
+            *reinterpret_cast<f32x4*>(a + 4 * (c + g)) = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+}
+
+// dQ = BF16(fl32(alpha A)) from the FP32 accumulator, 4 elements per thread.
+__global__ __launch_bounds__(256) void bwd_dq_finalize_kernel(const float* __restrict__ dQacc,
+                                                              uint16_t* __restrict__ dQ,
+                                                              size_t quads, float scale) {
+    const size_t t = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= quads) return;
+    const f32x4 a = *reinterpret_cast<const f32x4*>(dQacc + 4 * t);
+    float v[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma clang fp contract(off)
+        v[i] = scale * a[i];
+    }
+    st_bf16x4(dQ + 4 * t, v[0], v[1], v[2], v[3]);
+}
+
 }  // namespace
+
+hipError_t launch_bwd_pre(const uint16_t* O, const uint16_t* dO, const float* LSE, float* TS,
+                          float* dQacc, const Shape& s, hipStream_t st) {
+    const int T = (s.N + kTile - 1) / kTile;
+    dim3 grid((unsigned)(s.BH * T)), block(kThreads);
+    if (s.d == 64)
+        bwd_pre_kernel<64><<<grid, block, 0, st>>>(O, dO, LSE, TS, dQacc, s.BH, s.N);
+    else
+        bwd_pre_kernel<128><<<grid, block, 0, st>>>(O, dO, LSE, TS, dQacc, s.BH, s.N);
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_fused_plain(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                                  const uint16_t* dO, const float* TS, uint16_t* dK, uint16_t* dV,
+                                  float* dQacc, const Shape& s, hipStream_t st) {
+    const int Tk = (s.N + kTile - 1) / kTile;
+    dim3 grid((unsigned)(s.BH * Tk)), block(kThreads);
+    if (s.d == 64)
+        bwd_dkdv_kernel<64, false, true><<<grid, block, 0, st>>>(
+            Q, K, V, dO, TS, nullptr, dK, dV, nullptr, nullptr, s.BH, s.N, s.causal, s.scale, 1,
+            nullptr, s.BH, 0, nullptr, 0, s.N, dQacc);
+    else
+        bwd_dkdv_kernel<128, false, true><<<grid, block, 0, st>>>(
+            Q, K, V, dO, TS, nullptr, dK, dV, nullptr, nullptr, s.BH, s.N, s.causal, s.scale, 1,
+            nullptr, s.BH, 0, nullptr, 0, s.N, dQacc);
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_dq_finalize(const float* dQacc, uint16_t* dQ, const Shape& s,
+                                  hipStream_t st) {
+    const size_t quads = (size_t)s.BH * s.N * s.d / 4;
+    dim3 grid((unsigned)((quads + 255) / 256)), block(256);
+    bwd_dq_finalize_kernel<<<grid, block, 0, st>>>(dQacc, dQ, quads, s.scale);
+    return hipGetLastError();
+}
 
 hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                          const uint16_t* O, const uint16_t* dO, const float* LSE, float* Drow,

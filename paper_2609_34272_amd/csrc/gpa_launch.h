@@ -37,7 +37,10 @@ enum KernelId {
     kKF32Dq = 4,
     kKF32Dkdv = 5,
     kKGroupSum = 6,
-    kNumKernels = 7
+    kKBwdPre = 7,
+    kKBwdFused = 8,
+    kKBwdFinal = 9,
+    kNumKernels = 10
 };
 
 // fma_forward selects the historical exponent rounding (diagnostic only).
@@ -62,6 +65,20 @@ hipError_t launch_bwd_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t*
                            const uint16_t* dO, const float* TS, const uint16_t* Z,
                            uint16_t* dK, uint16_t* dV, float* dKp, float* dVp, int mode,
                            const Shape& s, hipStream_t st);
+
+// Single key-major plain backward with FP32 atomic dQ (dense multi-head):
+// launch_bwd_pre writes the per-tile statistics TS ([BH, T, 2, 64], as the
+// query-major pass does, same D bits) and zeroes dQacc ([BH, N, d] FP32);
+// launch_bwd_fused_plain writes dK, dV (the plain key pass's arithmetic) and
+// adds t K into dQacc with atomics; launch_bwd_dq_finalize writes
+// dQ = BF16(scale * dQacc).
+hipError_t launch_bwd_pre(const uint16_t* O, const uint16_t* dO, const float* LSE, float* TS,
+                          float* dQacc, const Shape& s, hipStream_t st);
+hipError_t launch_bwd_fused_plain(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                                  const uint16_t* dO, const float* TS, uint16_t* dK, uint16_t* dV,
+                                  float* dQacc, const Shape& s, hipStream_t st);
+hipError_t launch_bwd_dq_finalize(const float* dQacc, uint16_t* dQ, const Shape& s,
+                                  hipStream_t st);
 
 // dK = BF16(scale * sum_g dKp), dV = BF16(sum_g dVp) over the G query heads of
 // each key/value head, in head order.
