@@ -91,7 +91,7 @@ gpa_status gpa_attn_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
  * shapes, 0 for invalid arguments).  The caller allocates it; its contents on
  * entry do not matter.  It holds the FP32 row statistics D, rho, m, lambda
  * ([B,H,N] each), a per-64-row-tile copy of log2-scaled LSE and D for the
- * key-major pass, and in gproj mode the BF16 [B,H,N,d] tensor z = BF16(lambda q).
+ * key-major pass, and in gproj mode the BF16 [B,H,N,d] tensor -z = BF16(-lambda q).
  */
 size_t gpa_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d, int mode);
 
@@ -110,7 +110,8 @@ size_t gpa_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d, 
  *             m = rowsum(r); dQ = BF16( fl32[scale (tK - lambda rK)] );
  *             dK, dV bitwise equal to plain
  *   gproj   : as gproj_q, and dK = BF16( fl32[scale (t^T Q - r^T z)] ),
- *             z_i = BF16(lambda_i q_i); dQ, dV bitwise equal to gproj_q
+ *             z_i = BF16(lambda_i q_i), with t^T Q and r^T (-z) added into
+ *             one FP32 accumulator; dQ, dV bitwise equal to gproj_q
  * All FP32 accumulations are over BF16 products.  The schedule is
  * deterministic: repeated calls give bitwise identical results.
  * workspace: device buffer of at least gpa_attn_bwd_workspace_bytes(...)

@@ -118,7 +118,7 @@ struct BwdLayout {
 // query tile a 512-byte block of log2-scaled LSE and D (FP32 [problems, T, 2,
 // 64], T = the longest sequence rounded up to 64, over 64) that the key-major
 // pass stages with the tile; then (gproj mode only) the BF16 tensor
-// z = BF16(lambda q), shaped like Q, that the key correction contracts; then,
+// -z = BF16(-lambda q), shaped like Q, that the key correction contracts; then,
 // for grouped-query attention (Hq > Hkv) only, the FP32 per-query-head
 // contributions to dK and dV (Hq heads over the key rows) that the group sum
 // adds.

@@ -14,9 +14,11 @@
 //                  It also forms D_i = rowsum(dO_i * O_i) (FP32) for its rows,
 //                  and in gproj mode writes z = BF16(lambda q), once per row.
 //   2. bwd_dkdv  : key-major.  A workgroup owns 64 keys and streams the query
-//                  tiles (Q, dO and z); it accumulates dV = r^T dO,
-//                  dK^acc = t^T Q and C = r^T z and writes
-//                  dK = BF16(fl32[alpha (dK^acc - C)]).
+//                  tiles (Q, dO and -z); it accumulates dV = r^T dO and, in one
+//                  FP32 accumulator, dK^acc - C = t^T Q + r^T (-z), and writes
+//                  dK = BF16(fl32[alpha (dK^acc - C)]).  (The paper keeps two
+//                  accumulators and subtracts them; one accumulator holds the
+//                  same BF16 products summed in another FP32 order.)
 // Both passes rebuild P, r and t with identical instructions, so the r and t
 // of the key pass equal those of the query pass bitwise, and lambda is divided
 // once.  gproj_q runs the GProj query pass and the plain key pass; gproj runs
@@ -356,13 +358,16 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
                 st_bf16x4(drow + mb * 16 + 4 * g, v[0], v[1], v[2], v[3]);
             }
             if (WRITE_Z) {
-                // z = BF16(fl32(lambda q)) for the key correction: the lane holds
-                // d = kc*32 + 8g .. +7 of its query row.
+                // -z = BF16(fl32(-lambda q)) = -BF16(fl32(lambda q)) for the key
+                // correction (negation is exact), so the key pass adds r^T (-z)
+                // into the t^T Q accumulator: the lane holds d = kc*32 + 8g .. +7
+                // of its query row.
 #pragma unroll
                 for (int kc = 0; kc < KC; ++kc) {
                     bf16x8 z;
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) z[e] = to_bf16(lam * bf16_to_f32(qf[nb][kc][e]));
+                    for (int e = 0; e < 8; ++e)
+                        z[e] = to_bf16(-lam * bf16_to_f32(qf[nb][kc][e]));
                     *reinterpret_cast<bf16x8*>(Zout + hoff + (size_t)qrow * D + kc * 32 + 8 * g) = z;
                 }
             }
@@ -428,7 +433,9 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     constexpr int MB = D / 16;
     constexpr int KC = D / 32;
     constexpr int NT = GPROJ ? 3 : 2;  // staged tensors: Q, dO (and Z = BF16(lambda Q))
-    constexpr int NV = GPROJ ? 3 : 2;  // accumulators per output element: dV, dK^acc (, C)
+    // Accumulators per output element: dV, and dK^acc - C in one (the GProj
+    // pass adds t^T Q and r^T (-z) into the same FP32 accumulator).
+    constexpr int NV = 2;
     constexpr int PER_KB = NV * MB * 4;
     // One ring slot: the NT query-tile tensors, then per wave the row
     // statistics of its 32 queries (32 log2-LSE, 32 D as FP32).  Three slots in
@@ -482,7 +489,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
         }
     const float c = scale * kLog2e;
 
-    f32x4 accV[2][MB], accK[2][MB], accC[2][GPROJ ? MB : 1];
+    f32x4 accV[2][MB], accK[2][MB];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
@@ -490,8 +497,6 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
             accV[kb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
             accK[kb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
-#pragma unroll
-        for (int mb = 0; mb < (GPROJ ? MB : 1); ++mb) accC[kb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
 
     // The first query tile that sees a key of this tile.  The causal boundary
@@ -622,7 +627,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
             for (int kb = 0; kb < 2; ++kb) {
                 accV[kb][mb] = mfma_16x16x32(ua, rf[kb], accV[kb][mb]);
                 accK[kb][mb] = mfma_16x16x32(qa, tf[kb], accK[kb][mb]);
-                if (GPROJ) accC[kb][mb] = mfma_16x16x32(za, rf[kb], accC[kb][mb]);
+                if (GPROJ) accK[kb][mb] = mfma_16x16x32(za, rf[kb], accK[kb][mb]);
             }
             if (mb + 2 < MB) read_ops(opd[mb & 1], mb + 2);
             fill_piece(nxt2, qt + 2, AT_START + 4 + mb);
@@ -705,7 +710,6 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
                 const int j = (mb * 4 + i) * NV;
                 red[kb][j] = accV[kb][mb][i];
                 red[kb][j + 1] = accK[kb][mb][i];
-                if (GPROJ) red[kb][j + NV - 1] = accC[kb][mb][i];
             }
         if (kb) __syncthreads();  // the previous exchange has been read
         pair_reduce<PER_KB, sizeof(B0) / 4>(red[kb], reinterpret_cast<float*>(B0), wave, lane);
@@ -728,7 +732,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
 #pragma clang fp contract(off)
                     const int j = (mb * 4 + i) * NV;
                     dv[i] = red[kb][j];
-                    dk[i] = GPROJ ? red[kb][j + 1] - red[kb][j + NV - 1] : red[kb][j + 1];
+                    dk[i] = red[kb][j + 1];
                 }
                 *reinterpret_cast<f32x4*>(vp + mb * 16 + 4 * g) = dv;
                 *reinterpret_cast<f32x4*>(kp + mb * 16 + 4 * g) = dk;
@@ -745,12 +749,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
 #pragma clang fp contract(off)
                 const int j = (mb * 4 + i) * NV;
                 dv[i] = red[kb][j];
-                if (GPROJ) {
-                    const float diff = red[kb][j + 1] - red[kb][j + NV - 1];
-                    dk[i] = scale * diff;
-                } else {
-                    dk[i] = scale * red[kb][j + 1];
-                }
+                dk[i] = scale * red[kb][j + 1];
             }
             st_bf16x4(vrow + mb * 16 + 4 * g, dv[0], dv[1], dv[2], dv[3]);
             st_bf16x4(krw + mb * 16 + 4 * g, dk[0], dk[1], dk[2], dk[3]);

@@ -48,7 +48,7 @@ hipError_t launch_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, u
                       float* LSE, const Shape& s, hipStream_t st, bool fma_forward = false);
 
 // Query-major pass: writes D = rowsum(dO * O) and dQ; in the gproj modes also
-// rho, m, lambda (zero in plain mode); in gproj mode also Z = BF16(lambda Q)
+// rho, m, lambda (zero in plain mode); in gproj mode also Z = BF16(-lambda Q)
 // ([BH, N, d], BF16).  TS ([BH, T, 2, 64] FP32, T = tiles of 64 rows)
 // receives per tile LSE * log2(e) (+inf beyond N) and D (0 beyond N) for the
 // key pass.
