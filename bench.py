@@ -53,7 +53,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-accuracy", action="store_true")
     p.add_argument("--no-configs", action="store_true",
-                   help="skip the timing of the d = 128 and batched workloads")
+                   help="skip the timing of the d = 128, long-sequence and batched workloads")
     p.add_argument("--no-seeds", action="store_true",
                    help="skip the 8-seed accuracy protocol of the reference workload")
     p.add_argument("--no-gqa", action="store_true",
@@ -423,13 +423,13 @@ def main():
     if gqa is not None:
         out["gqa"] = gqa
 
-    # The wider-head and batched workloads, timed on the same kernels (their
-    # parity is covered by the tests): forward and backward per mode, the GProj
-    # overhead and each kernel's fraction of the bf16 peak by its algorithmic
-    # products.
+    # The wider-head, long-sequence and batched workloads, timed on the same
+    # kernels (their parity is covered by the tests): forward and backward per
+    # mode, the GProj overhead and each kernel's fraction of the bf16 peak by
+    # its algorithmic products.
     if not args.no_configs and w.name == "h16_n4096_d64":
         out["configs"] = {}
-        for idx, iters in ((3, 50), (5, 6)):
+        for idx, iters in ((3, 50), (4, 20), (5, 6)):
             wc = S.WORKLOADS[idx]
             out["configs"][wc.name] = time_config(gpa, S, wc, 1000 * idx, iters, dev, to_dev)
 
