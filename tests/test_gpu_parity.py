@@ -476,3 +476,49 @@ def test_seed_protocol_medians():
               + " ".join(f"{v:.4f}" for v in o))
         med = {n: np.median([SEED_LOG[wl][s]["gproj"][n] for s in seeds]) for n in NAMES}
         assert all(v <= 1.0 for v in med.values()), (wl, med)
+
+
+# ------------------------------------ both passes form the same t and r
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_both_passes_form_the_same_t_and_r(gpa, causal):
+    """The query-major and key-major passes rebuild P, t and r independently.
+    With d = 128, N = 64, Q = [I | X] and K = [Y | I] the logits q_i.k_j =
+    y_j[i] + x_i[j] are arbitrary, yet every product the kernels form reads
+    single values of t and r exactly: A_i (query pass) holds t_ij at column
+    64 + j, dK^acc_j (key pass) holds t_ij at column i, and with dO = [I | 0]
+    dV_j holds r_ij at column i.  With alpha = 1/8 every cast is exact, so
+    plain dQ and dK must give the same t bit for bit, and gproj_q's dQ =
+    BF16(fl32[alpha (t - lambda r)]) must match the key pass's r."""
+    N, d, alpha = 64, 128, 0.125
+    rng = np.random.default_rng(12)
+    eye = np.eye(N, dtype=np.float32)
+    X = S.bf16_bits_to_f32(S.f32_to_bf16_bits(rng.standard_normal((N, N)).astype(np.float32)))
+    Y = S.bf16_bits_to_f32(S.f32_to_bf16_bits(rng.standard_normal((N, N)).astype(np.float32)))
+    q = np.concatenate([eye, X], axis=1)[None, None]
+    k = np.concatenate([Y, eye], axis=1)[None, None]
+    v = rng.standard_normal((1, 1, N, d)).astype(np.float32)
+    u = np.concatenate([eye, np.zeros((N, N), np.float32)], axis=1)[None, None]
+    x = {n: S.f32_to_bf16_bits(a) for n, a in zip(("q", "k", "v", "do"), (q, k, v, u))}
+    qd, kd, vd, ud = (G.to_dev(x[n]) for n in ("q", "k", "v", "do"))
+    o, lse = gpa.attn_fwd(qd, kd, vd, causal, alpha)
+    dq, dk, dv = gpa.attn_bwd(qd, kd, vd, o, lse, ud, "plain", causal, alpha)
+    dq_g, _, dv_g, st = gpa.attn_bwd(qd, kd, vd, o, lse, ud, "gproj_q", causal, alpha,
+                                     return_stats=True)
+    torch.cuda.synchronize()
+    DQ, DK, DV = (G.to_host(t)[0, 0].astype(np.float32) for t in (dq, dk, dv))
+    t_query = DQ[:, N:] / np.float32(alpha)          # t_ij from the query pass
+    t_key = DK[:, :N].T / np.float32(alpha)          # t_ij from the key pass
+    r_key = DV[:, :N].T                              # r_ij from the key pass
+    assert np.array_equal(t_query, t_key)
+    assert np.count_nonzero(t_query) > N              # a non-trivial pattern
+    lam = st["lambda"][0, 0].cpu().numpy().astype(np.float32)
+    a32 = np.float32(alpha)
+    corr = (lam[:, None] * r_key).astype(np.float32)
+    want = (a32 * (t_query - corr).astype(np.float32)).astype(np.float32)
+    want_bits = S.f32_to_bf16_bits(want)
+    got_bits = G.bits(dq_g)[0, 0][:, N:]
+    assert np.array_equal(got_bits, want_bits)
+    assert np.array_equal(G.bits(dv_g), G.bits(dv))
+    G.log(f"[t and r across passes, causal={causal}] {np.count_nonzero(t_query)} nonzero t, "
+          f"{np.count_nonzero(r_key)} nonzero r: identical in both passes")
