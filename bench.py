@@ -287,10 +287,16 @@ def main():
     gpa.profile_enable(False)
     atomic_kern = {n: round(t / c, 5) for n, (t, c) in aprof.items() if c}
     fwd_ms = timed(lambda: gpa.attn_fwd(q, k, v, w.causal, w.scale), args.steps)
-    # The same K steps timed again, now that the sections above have kept the
-    # GPU busy: the part raises its clock over the first tens of milliseconds
-    # of load, so with few warmup steps `ms_per_step` includes that ramp.
-    ms_again = timed(lambda: step(args.mode), args.steps)
+    # Reference only (not `value`): the same K steps timed after 200 further
+    # steps of this workload.  From idle the part runs its first milliseconds
+    # at a boost clock and then throttles for several milliseconds before it
+    # settles (kernel traces show the key pass at ~91 us in the first steps,
+    # 100-110 us in the next ones and ~88 us once settled), and each switch to
+    # another heavy workload starts a new transient; a short run times the
+    # transient, a training loop runs at the settled clock.
+    for _ in range(200):
+        step(args.mode)
+    ms_steady = timed(lambda: step(args.mode), args.steps)
 
     # Per-call distribution (p10 / median / p90 ms): each call bracketed by its
     # own pair of events, so each figure carries a few microseconds of event
@@ -418,7 +424,7 @@ def main():
         "fp32_attn": fp32,
         "fp32_attn_vs_gproj_fwd_bwd": round(fp32_ms / (fwd_ms + bwd_ms["gproj"]), 3),
         "wall_s_timed": round(wall, 3),
-        "ms_per_step_retimed_after_load": round(ms_again, 5),
+        "ms_per_step_steady_after_200_more_steps": round(ms_steady, 5),
     }
     if gqa is not None:
         out["gqa"] = gqa
