@@ -92,15 +92,18 @@ def recorded_traffic(kernel: str, mode: str, workload: str = "h16_n4096_d64"):
     return None if k is None else k.get("hbm_bytes_per_launch")
 
 
-def time_config(gpa, S, wc, seed, iters, dev, to_dev):
+def time_config(gpa, S, wc, seed, iters, dev, to_dev, oracle=None, heads=None):
     """Forward and per-mode backward times of one multi-head workload (mean of
     `iters` calls after ~100 ms of load), its fwd+bwd TFLOP/s by the standard
     count, the GProj overhead and every kernel's fraction of the bf16 peak by
-    its algorithmic products."""
+    its algorithmic products.  With the oracle, also the relative L2 errors
+    (%) of O, dQ, dK, dV in every mode and of the FP32 baseline against the
+    FP64 VJP, over the whole tensors or over the listed (b, h) heads."""
     import torch
     xc = S.make_inputs(wc, seed, workers=16)
     q, k, v, u = (to_dev(xc[n]) for n in ("q", "k", "v", "do"))
-    del xc
+    if oracle is None:
+        del xc
     B, H, N, d = wc.B, wc.H, wc.N, wc.d
 
     def timed(fn):
@@ -165,6 +168,28 @@ def time_config(gpa, S, wc, seed, iters, dev, to_dev):
         100.0 * (res["bwd_ms"]["gproj"] / res["bwd_ms"]["plain"] - 1), 2)
     res["gproj_q_bwd_overhead_vs_plain_pct"] = round(
         100.0 * (res["bwd_ms"]["gproj_q"] / res["bwd_ms"]["plain"] - 1), 2)
+    if oracle is not None:
+        import numpy as np
+        sel = list(heads) if heads else [(b, h) for b in range(B) for h in range(H)]
+        bi = torch.tensor([b for b, _ in sel], device=dev)
+        hi = torch.tensor([h for _, h in sel], device=dev)
+        host = lambda t: t[bi, hi].float().cpu().numpy().astype(np.float64)  # noqa: E731
+        outs = {}
+        for m in gpa.MODES:
+            dq, dk, dv = gpa.attn_bwd(q, k, v, o, lse, u, m, wc.causal, wc.scale)
+            outs[m] = [host(t) for t in (o, dq, dk, dv)]
+            del dq, dk, dv
+        fo, _, fdq, fdk, fdv = gpa.fp32_attn(q, k, v, u, wc.causal, wc.scale)
+        outs["fp32"] = [host(t) for t in (fo, fdq, fdk, fdv)]
+        del fo, fdq, fdk, fdv
+        pick = lambda a: np.stack([a[b, h] for b, h in sel])  # noqa: E731
+        ex = oracle.exact(pick(xc["q"]), pick(xc["k"]), pick(xc["v"]), pick(xc["do"]), wc.causal,
+                          wc.scale)
+        res["rel_l2_pct_vs_fp64"] = {
+            "heads": "all" if not heads else [list(p) for p in sel],
+            **{m: {n: round(oracle.rel_l2(t, ex[n]), 4) for n, t in zip(("O", "dQ", "dK", "dV"), ts)}
+               for m, ts in outs.items()}}
+        del xc
     del q, k, v, u, o, lse
     torch.cuda.empty_cache()
     return res
@@ -435,9 +460,15 @@ def main():
     # its algorithmic products.
     if not args.no_configs and w.name == "h16_n4096_d64":
         out["configs"] = {}
+        orc = None
+        if not args.no_accuracy:
+            import oracle as orc
         for idx, iters in ((3, 50), (4, 20), (5, 6)):
             wc = S.WORKLOADS[idx]
-            out["configs"][wc.name] = time_config(gpa, S, wc, 1000 * idx, iters, dev, to_dev)
+            out["configs"][wc.name] = time_config(
+                gpa, S, wc, 1000 * idx, iters, dev, to_dev,
+                oracle=orc,
+                heads=None if idx == 3 else ([(0, 0), (0, 15)] if idx == 4 else [(0, 0), (7, 31)]))
 
     if not args.no_accuracy or not args.no_cpu_baseline:
         import oracle
