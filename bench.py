@@ -296,21 +296,27 @@ def main():
             gpa.attn_bwd(q, k, v, o, lse, u, m, w.causal, w.scale, workspace=ws[m])
         bwd_ms[m] = timed(lambda: gpa.attn_bwd(q, k, v, o, lse, u, m, w.causal, w.scale,
                                                workspace=ws[m]), args.steps)
-    # The plain backward as one key-major pass with FP32 atomic dQ (Algorithm
-    # 1's first loop): the other candidate for the fastest plain backward.
-    wsa = torch.empty(gpa.attn_bwd_atomic_workspace_bytes(B, H, N, d), dtype=torch.uint8,
-                      device=dev)
-    fa = lambda: gpa.attn_bwd_atomic(q, k, v, o, lse, u, w.causal, w.scale, workspace=wsa)  # noqa: E731
-    for _ in range(3):
-        fa()
-    bwd_ms["plain_atomic_dq"] = timed(fa, args.steps)
-    gpa.profile_enable(True)
-    for _ in range(max(5, args.steps // 5)):
-        fa()
-    torch.cuda.synchronize()
-    aprof = gpa.profile_read()
-    gpa.profile_enable(False)
-    atomic_kern = {n: round(t / c, 5) for n, (t, c) in aprof.items() if c}
+    # Algorithm 1's own schedule (one key-major pass with FP32 atomic
+    # accumulation of the query-side sums; gproj adds the key-correction
+    # pass): for plain the other candidate for the fastest plain backward, for
+    # the GProj modes the literal schedule beside the two-pass one.
+    atomic_kern = {}
+    for m in gpa.MODES:
+        wsa = torch.empty(gpa.attn_bwd_atomic_workspace_bytes(B, H, N, d, m), dtype=torch.uint8,
+                          device=dev)
+        fa = lambda: gpa.attn_bwd_atomic(q, k, v, o, lse, u, m, w.causal, w.scale,  # noqa: E731
+                                         workspace=wsa)
+        for _ in range(3):
+            fa()
+        bwd_ms["plain_atomic_dq" if m == "plain" else m + "_atomic"] = timed(fa, args.steps)
+        gpa.profile_enable(True)
+        for _ in range(max(5, args.steps // 5)):
+            fa()
+        torch.cuda.synchronize()
+        aprof = gpa.profile_read()
+        gpa.profile_enable(False)
+        atomic_kern[m] = {n: round(t / c, 5) for n, (t, c) in aprof.items() if c}
+        del wsa
     fwd_ms = timed(lambda: gpa.attn_fwd(q, k, v, w.causal, w.scale), args.steps)
     # Reference only (not `value`): the same K steps timed after 200 further
     # steps of this workload.  From idle the part runs its first milliseconds
@@ -443,7 +449,8 @@ def main():
         # overheads against the fastest plain backward measured here (the
         # two-pass schedule or the single pass with atomic dQ)
         "best_plain": best_plain,
-        "plain_atomic_dq_kernels_ms": atomic_kern,
+        "plain_atomic_dq_kernels_ms": atomic_kern["plain"],
+        "atomic_schedule_kernels_ms": {m: atomic_kern[m] for m in ("gproj_q", "gproj")},
         "gproj_bwd_overhead_vs_plain_pct": round(100.0 * (bwd_ms["gproj"] / bwd_ms[best_plain] - 1), 2),
         "gproj_q_bwd_overhead_vs_plain_pct": round(100.0 * (bwd_ms["gproj_q"] / bwd_ms[best_plain] - 1), 2),
         "fp32_attn": fp32,

@@ -154,25 +154,36 @@ gpa_status gpa_attn_bwd_noalloc(const uint16_t* Q, const uint16_t* K, const uint
                                 int causal, float scale, int mode, void* stream);
 
 /*
- * Plain backward as one key-major pass with FP32 atomic dQ (Algorithm 1's
- * first loop without the GProj additions: dQ accumulated by atomic adds while
- * dK and dV stay with their key tile), for measurement beside the two-pass
- * schedule gpa_attn_bwd uses.  Dense multi-head only; arguments as
- * gpa_attn_bwd in plain mode.  Three kernels: D and the per-tile statistics
- * (bitwise those of gpa_attn_bwd's query-major pass) with the FP32 dQ
- * accumulator zeroed; the key-major pass, whose dK and dV are bitwise those of
- * gpa_attn_bwd in plain mode and which adds each tile's t K into the
- * accumulator with device-scope FP32 atomics; dQ = BF16(fl32(scale A)).  The
- * atomic order varies between runs, so dQ is not bitwise reproducible (its
- * FP32 sums are the same terms in another order).  workspace: at least
- * gpa_attn_bwd_atomic_workspace_bytes(...) bytes, 256-byte aligned.
+ * The backward with Algorithm 1's own schedule (dense multi-head; arguments as
+ * gpa_attn_bwd), for measurement beside the two-pass schedule gpa_attn_bwd
+ * uses: one key-major pass in which dK and dV stay with their key tile while
+ * the query-side sums are added into FP32 accumulators with device-scope
+ * atomics.  Kernels, in stream order:
+ *   1. D and the per-tile statistics (bitwise those of gpa_attn_bwd's
+ *      query-major pass), accumulators zeroed;
+ *   2. the key-major pass (Algorithm 1's first loop): dV, and dK (plain,
+ *      gproj_q: bitwise gpa_attn_bwd's) or the FP32 dK^acc = t^T Q (gproj);
+ *      A = tK by atomics, and in the GProj modes also B = rK and the row
+ *      masses rho = sum t, m = sum r (eq. gproj-row-mass);
+ *   3. dQ = BF16(fl32(scale A)) (plain), or lambda = rho/m and
+ *      dQ = BF16(fl32[scale (A - lambda B)]) (eq. gproj-query-implemented),
+ *      with -z = BF16(-lambda q) in gproj mode;
+ *   4. gproj mode only, the second key-major pass (Algorithm 1's correction
+ *      loop): r-tilde rebuilt (bitwise the first pass's r), C = r-tilde^T z,
+ *      dK = BF16(fl32[scale (dK^acc - C)]) (eq. gproj-key-implemented).
+ * dV is bitwise that of gpa_attn_bwd in every mode.  The atomic order varies
+ * between runs, so dQ (and through lambda the gproj dK) is not bitwise
+ * reproducible: its FP32 sums hold the same terms in another order.
+ * workspace: at least gpa_attn_bwd_atomic_workspace_bytes(..., mode) bytes,
+ * 256-byte aligned (0 for an invalid shape or mode).  Errors as gpa_attn_bwd.
  */
-size_t gpa_attn_bwd_atomic_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d);
+size_t gpa_attn_bwd_atomic_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d,
+                                           int mode);
 gpa_status gpa_attn_bwd_atomic(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                                const uint16_t* O, const float* LSE, const uint16_t* dO,
                                uint16_t* dQ, uint16_t* dK, uint16_t* dV,
                                int64_t B, int64_t H, int64_t N, int64_t d,
-                               int causal, float scale,
+                               int causal, float scale, int mode,
                                void* workspace, size_t workspace_bytes, void* stream);
 
 /*

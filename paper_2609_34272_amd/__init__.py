@@ -99,10 +99,10 @@ def lib():
     L.gpa_attn_bwd_noalloc.argtypes = [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, INT, F32,
                                        INT, P]
     L.gpa_attn_bwd_atomic_workspace_bytes.restype = SZ
-    L.gpa_attn_bwd_atomic_workspace_bytes.argtypes = [I64, I64, I64, I64]
+    L.gpa_attn_bwd_atomic_workspace_bytes.argtypes = [I64, I64, I64, I64, INT]
     L.gpa_attn_bwd_atomic.restype = INT
-    L.gpa_attn_bwd_atomic.argtypes = [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, INT, F32, P,
-                                      SZ, P]
+    L.gpa_attn_bwd_atomic.argtypes = [P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, INT, F32, INT,
+                                      P, SZ, P]
     L.gpa_profile_read.restype = INT
     L.gpa_profile_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64), INT]
     L.gpa_kernel_name.restype = ctypes.c_char_p
@@ -243,27 +243,32 @@ def attn_bwd(q, k, v, o, lse, do, mode: str = "gproj", causal: bool = True, scal
     return dq, dk, dv, stats
 
 
-def attn_bwd_atomic(q, k, v, o, lse, do, causal: bool = True, scale=None, workspace=None):
-    """Plain backward as one key-major pass with FP32 atomic dQ
-    (gpa_attn_bwd_atomic; dense multi-head).  dK, dV bitwise those of
-    attn_bwd(mode="plain"); dQ the same sums in another order."""
+def attn_bwd_atomic(q, k, v, o, lse, do, mode: str = "plain", causal: bool = True, scale=None,
+                    workspace=None):
+    """The backward with Algorithm 1's schedule: one key-major pass with FP32
+    atomic accumulation of the query-side sums, then (gproj) the key
+    correction pass (gpa_attn_bwd_atomic; dense multi-head).  dV bitwise that
+    of attn_bwd(mode=mode); plain and gproj_q dK too; dQ the same sums in
+    another order."""
     B, H, N, d = _shape(q)
     for t, n in ((q, "q"), (k, "k"), (v, "v"), (o, "o"), (do, "do")):
         _need(t, n, (B, H, N, d), torch.bfloat16)
     _need(lse, "lse", (B, H, N), torch.float32)
-    nbytes = int(lib().gpa_attn_bwd_atomic_workspace_bytes(B, H, N, d))
+    mi = MODES[mode] if isinstance(mode, str) else int(mode)
+    nbytes = int(lib().gpa_attn_bwd_atomic_workspace_bytes(B, H, N, d, mi))
     if workspace is None:
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     _check(lib().gpa_attn_bwd_atomic(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
                                      lse.data_ptr(), do.data_ptr(), dq.data_ptr(), dk.data_ptr(),
                                      dv.data_ptr(), B, H, N, d, int(bool(causal)), _scale(d, scale),
-                                     workspace.data_ptr(), workspace.numel(), _stream(q)))
+                                     mi, workspace.data_ptr(), workspace.numel(), _stream(q)))
     return dq, dk, dv
 
 
-def attn_bwd_atomic_workspace_bytes(B: int, H: int, N: int, d: int) -> int:
-    return int(lib().gpa_attn_bwd_atomic_workspace_bytes(B, H, N, d))
+def attn_bwd_atomic_workspace_bytes(B: int, H: int, N: int, d: int, mode: str = "plain") -> int:
+    mi = MODES[mode] if isinstance(mode, str) else int(mode)
+    return int(lib().gpa_attn_bwd_atomic_workspace_bytes(B, H, N, d, mi))
 
 
 def attn_bwd_noalloc(q, k, v, o, lse, do, mode: str = "gproj", causal: bool = True, scale=None,

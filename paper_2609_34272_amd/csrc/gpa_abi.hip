@@ -109,6 +109,43 @@ gpa_status launched(hipError_t e, const char* what) {
     return GPA_OK;
 }
 
+// Workspace of the atomic schedule: the per-tile statistics block (as in
+// bwd_layout_rows), the FP32 [B,H,N,d] accumulator A; in the GProj modes the
+// FP32 accumulator B and the FP32 [B,H,N] row masses rho, m; in gproj mode
+// the FP32 [B,H,N,d] dK^acc and the BF16 -z shaped like Q.
+struct AtomicLayout {
+    size_t ts, a, b, rho, m, dkacc, z, total;
+};
+
+AtomicLayout atomic_layout(int64_t B, int64_t H, int64_t N, int64_t d, int mode) {
+    const size_t T = (size_t)(N + 63) / 64;
+    const size_t rows = (size_t)B * H * N;
+    const size_t big = round_up(rows * (size_t)d * sizeof(float));
+    const size_t row = round_up(rows * sizeof(float));
+    AtomicLayout l{};
+    size_t o = 0;
+    l.ts = o;
+    o += round_up((size_t)B * H * T * 128 * sizeof(float));
+    l.a = o;
+    o += big;
+    if (mode >= 1) {
+        l.b = o;
+        o += big;
+        l.rho = o;
+        o += row;
+        l.m = o;
+        o += row;
+    }
+    if (mode == 2) {
+        l.dkacc = o;
+        o += big;
+        l.z = o;
+        o += round_up(rows * (size_t)d * 2);
+    }
+    l.total = o;
+    return l;
+}
+
 struct BwdLayout {
     size_t D, rho, m, lam, ts, z, dkp, dvp, total;
 };
@@ -455,22 +492,23 @@ gpa_status gpa_attn_bwd_noalloc(const uint16_t* Q, const uint16_t* K, const uint
                    (size_t)B * H * N, mode, ws, (hipStream_t)stream);
 }
 
-size_t gpa_attn_bwd_atomic_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d) {
-    if (B < 1 || H < 1 || N < 1 || (d != 64 && d != 128)) return 0;
+size_t gpa_attn_bwd_atomic_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d,
+                                           int mode) {
+    if (B < 1 || H < 1 || N < 1 || (d != 64 && d != 128) || mode < 0 || mode > 2) return 0;
     if ((double)B * H * N * d >= 2147483648.0) return 0;
-    const size_t T = (size_t)(N + 63) / 64;
-    return round_up((size_t)B * H * T * 128 * sizeof(float)) +
-           round_up((size_t)B * H * N * d * sizeof(float));
+    const AtomicLayout l = atomic_layout(B, H, N, d, mode);
+    return l.total;
 }
 
 gpa_status gpa_attn_bwd_atomic(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
                                const uint16_t* O, const float* LSE, const uint16_t* dO,
                                uint16_t* dQ, uint16_t* dK, uint16_t* dV, int64_t B, int64_t H,
-                               int64_t N, int64_t d, int causal, float scale, void* workspace,
-                               size_t workspace_bytes, void* stream) {
+                               int64_t N, int64_t d, int causal, float scale, int mode,
+                               void* workspace, size_t workspace_bytes, void* stream) {
     gpa_status s = check_shape(B, H, N, d, scale);
     if (s != GPA_OK) return s;
-    const size_t need = gpa_attn_bwd_atomic_workspace_bytes(B, H, N, d);
+    if (mode < 0 || mode > 2) return fail(GPA_EINVAL, "mode %d is not 0, 1 or 2", mode);
+    const size_t need = gpa_attn_bwd_atomic_workspace_bytes(B, H, N, d, mode);
     if (!workspace || workspace_bytes < need)
         return fail(GPA_EWORKSPACE, "workspace %p of %zu bytes; %zu needed", workspace,
                     workspace_bytes, need);
@@ -483,22 +521,45 @@ gpa_status gpa_attn_bwd_atomic(const uint16_t* Q, const uint16_t* K, const uint1
     if (s != GPA_OK) return s;
     const gpa::Shape sh{(int)(B * H), (int)N, (int)d, causal ? 1 : 0, scale, 1};
     hipStream_t st = (hipStream_t)stream;
-    const size_t T = (size_t)(N + 63) / 64;
-    float* TS = (float*)workspace;
-    float* acc = (float*)((char*)workspace + round_up((size_t)B * H * T * 128 * sizeof(float)));
+    const AtomicLayout l = atomic_layout(B, H, N, d, mode);
+    char* w = (char*)workspace;
+    float* TS = (float*)(w + l.ts);
+    gpa::AtomicAcc acc;
+    acc.A = (float*)(w + l.a);
+    if (mode >= 1) {
+        acc.B = (float*)(w + l.b);
+        acc.rho = (float*)(w + l.rho);
+        acc.m = (float*)(w + l.m);
+    }
+    if (mode == 2) acc.dKacc = (float*)(w + l.dkacc);
+    uint16_t* Zneg = mode == 2 ? (uint16_t*)(w + l.z) : nullptr;
     s = launched(timed(gpa::kKBwdPre, st,
                        [&] { return gpa::launch_bwd_pre(O, dO, LSE, TS, acc, sh, st); }),
                  "bwd_pre");
     if (s != GPA_OK) return s;
     s = launched(timed(gpa::kKBwdFused, st,
                        [&] {
-                           return gpa::launch_bwd_fused_plain(Q, K, V, dO, TS, dK, dV, acc, sh, st);
+                           return gpa::launch_bwd_fused(Q, K, V, dO, TS, dK, dV, acc, mode, sh,
+                                                        st);
                        }),
-                 "bwd_fused_plain");
+                 "bwd_fused");
     if (s != GPA_OK) return s;
-    return launched(timed(gpa::kKBwdFinal, st,
-                          [&] { return gpa::launch_bwd_dq_finalize(acc, dQ, sh, st); }),
-                    "bwd_dq_finalize");
+    if (mode == 0)
+        return launched(timed(gpa::kKBwdFinal, st,
+                              [&] { return gpa::launch_bwd_dq_finalize(acc.A, dQ, sh, st); }),
+                        "bwd_dq_finalize");
+    s = launched(timed(gpa::kKBwdFinal, st,
+                       [&] {
+                           return gpa::launch_bwd_gproj_finalize(acc, Q, dQ, Zneg, nullptr, sh,
+                                                                 st);
+                       }),
+                 "bwd_gproj_finalize");
+    if (s != GPA_OK || mode == 1) return s;
+    return launched(timed(gpa::kKBwdCorr, st,
+                          [&] {
+                              return gpa::launch_bwd_dk_corr(Q, K, TS, Zneg, acc.dKacc, dK, sh, st);
+                          }),
+                    "bwd_dk_corr");
 }
 
 gpa_status gpa_attn_fwd_varlen(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
@@ -642,7 +703,7 @@ int gpa_profile_read(double* total_ms, int64_t* launches, int n) {
 const char* gpa_kernel_name(int id) {
     static const char* names[gpa::kNumKernels] = {
         "fwd_sbs",   "bwd_dq",  "bwd_dkdv",        "fp32_fwd",       "fp32_dq",
-        "fp32_dkdv", "group_sum", "bwd_pre", "bwd_fused_plain", "bwd_dq_finalize"};
+        "fp32_dkdv", "group_sum", "bwd_pre", "bwd_fused", "bwd_dq_finalize", "bwd_dk_corr"};
     return (id >= 0 && id < gpa::kNumKernels) ? names[id] : "";
 }
 

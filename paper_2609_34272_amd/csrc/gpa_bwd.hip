@@ -415,12 +415,16 @@ __device__ __forceinline__ void dkdv_probs(const f32x4& s, const f32x4& dp, cons
     }
 }
 
-// FUSED_DQ (plain mode, dense multi-head only): the single key-major pass of
-// Algorithm 1's first loop without the GProj additions.  Besides dV and dK it
-// forms this key tile's share of A = tK for every query tile it visits and
-// adds it into the FP32 accumulator dQacc [BH, N, d] with device-scope atomic
-// adds (dQ = BF16(alpha A) is formed afterwards).  t goes through LDS once per
-// step, as the transposed operand of that product.
+// FUSED_DQ (dense multi-head only): the single key-major pass of Algorithm 1's
+// first loop.  Besides dV and dK it forms this key tile's share of A = tK for
+// every query tile it visits and adds it into the FP32 accumulator dQacc
+// [BH, N, d] with device-scope atomic adds (dQ is formed afterwards).  t goes
+// through LDS once per step, as the transposed operand of that product.  With
+// GPROJ as well it is that loop with the GProj additions: B = rK into Bacc
+// (r through LDS like t) and the row masses rho = sum t, m = sum r into
+// rho_acc, m_acc, all by atomic adds; the key correction is then a second
+// pass (bwd_dk_corr_kernel), so the FP32 dK^acc = t^T Q goes to dKacc
+// unscaled when dKacc is given (else dK = BF16(alpha dK^acc), as in plain).
 template <int D, bool GPROJ, bool FUSED_DQ = false>
 __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dkdv_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
@@ -428,11 +432,17 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     const float* __restrict__ TS, const uint16_t* __restrict__ Z, uint16_t* __restrict__ dK,
     uint16_t* __restrict__ dV, float* __restrict__ dKp, float* __restrict__ dVp, int BH, int Nmax,
     int causal, float scale, int G, const int* __restrict__ cu, int Hq, int total,
-    const int* __restrict__ cu_k, int total_k, int Nkmax, float* __restrict__ dQacc = nullptr) {
-    static_assert(!(FUSED_DQ && GPROJ), "the fused pass is the plain backward");
+    const int* __restrict__ cu_k, int total_k, int Nkmax, float* __restrict__ dQacc = nullptr,
+    float* __restrict__ Bacc = nullptr, float* __restrict__ rho_acc = nullptr,
+    float* __restrict__ m_acc = nullptr, float* __restrict__ dKacc = nullptr) {
     constexpr int MB = D / 16;
     constexpr int KC = D / 32;
-    constexpr int NT = GPROJ ? 3 : 2;  // staged tensors: Q, dO (and Z = BF16(lambda Q))
+    // ZC: the two-pass schedule's key correction, folded into this pass (Z
+    // staged, r^T (-z) added into the t^T Q accumulator).  AB: the atomic
+    // schedule's B, rho and m.
+    constexpr bool ZC = GPROJ && !FUSED_DQ;
+    constexpr bool AB = GPROJ && FUSED_DQ;
+    constexpr int NT = ZC ? 3 : 2;  // staged tensors: Q, dO (and Z = BF16(lambda Q))
     // Accumulators per output element: dV, and dK^acc - C in one (the GProj
     // pass adds t^T Q and r^T (-z) into the same FP32 accumulator).
     constexpr int NV = 2;
@@ -451,6 +461,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     // fused dQ: this tile's keys [key][d] and the step's t as [key][query]
     __shared__ __attribute__((aligned(16))) uint16_t Ks[FUSED_DQ ? TILE_E : 8];
     __shared__ __attribute__((aligned(16))) uint16_t Xt[FUSED_DQ ? kTile * kTile : 8];
+    __shared__ __attribute__((aligned(16))) uint16_t Xr[AB ? kTile * kTile : 8];
 
     const int Tq = (Nmax + kTile - 1) / kTile;   // query tiles of the longest problem
     const int Tk = (Nkmax + kTile - 1) / kTile;  // key tiles of the longest problem
@@ -507,7 +518,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     const uint16_t* src[NT];
     src[0] = Q + hoff;
     src[1] = dO + hoff;
-    if (GPROJ) src[NT - 1] = Z + hoff;
+    if (ZC) src[NT - 1] = Z + hoff;
 
     TileDma<D> dma;
     dma.init(lane, wave);
@@ -543,6 +554,9 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     }
     const rsrc_t rdq = make_rsrc(FUSED_DQ ? dQacc + hoff : nullptr,
                                  FUSED_DQ ? (uint32_t)N * (uint32_t)D * 4u : 0u);
+    const rsrc_t rdb = make_rsrc(AB ? Bacc + hoff : nullptr, AB ? (uint32_t)N * (uint32_t)D * 4u : 0u);
+    const rsrc_t rrho = make_rsrc(AB ? rho_acc + sr.q0 : nullptr, AB ? (uint32_t)N * 4u : 0u);
+    const rsrc_t rms = make_rsrc(AB ? m_acc + sr.q0 : nullptr, AB ? (uint32_t)N * 4u : 0u);
     fill(B0, qt0);
     fill(B1, qt0 + 1);
     wait_vm_lgkm0<FILL_VM>();
@@ -577,7 +591,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
         auto read_ops = [&](bf16x8 (&o)[NT], int mb) {
             o[0] = ld_tr_operand<D>(Uc, 32 * qh, mb * 16, c16, g);
             o[1] = ld_tr_operand<D>(Qc, 32 * qh, mb * 16, c16, g);
-            if (GPROJ) o[NT - 1] = ld_tr_operand<D>(Zc, 32 * qh, mb * 16, c16, g);
+            if (ZC) o[NT - 1] = ld_tr_operand<D>(Zc, 32 * qh, mb * 16, c16, g);
         };
         read_ops(opd[0], 0);
         read_ops(opd[1], 1);
@@ -627,38 +641,62 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
             for (int kb = 0; kb < 2; ++kb) {
                 accV[kb][mb] = mfma_16x16x32(ua, rf[kb], accV[kb][mb]);
                 accK[kb][mb] = mfma_16x16x32(qa, tf[kb], accK[kb][mb]);
-                if (GPROJ) accK[kb][mb] = mfma_16x16x32(za, rf[kb], accK[kb][mb]);
+                if (ZC) accK[kb][mb] = mfma_16x16x32(za, rf[kb], accK[kb][mb]);
             }
             if (mb + 2 < MB) read_ops(opd[mb & 1], mb + 2);
             fill_piece(nxt2, qt + 2, AT_START + 4 + mb);
         }
         if constexpr (FUSED_DQ) {
-            // t of this wave's 32 keys x 32 queries into Xt[key][query]: lane
-            // (c16, g) holds key 32 kh + 16 kb + c16 at queries 32 qh + 16 mq +
-            // 4 g + i, i.e. 8 contiguous bytes of one Xt row per (kb, mq).
+            // t of this wave's 32 keys x 32 queries into Xt[key][query] (r
+            // into Xr): lane (c16, g) holds key 32 kh + 16 kb + c16 at queries
+            // 32 qh + 16 mq + 4 g + i, i.e. 8 contiguous bytes of one Xt row
+            // per (kb, mq).  Keys beyond the key count (the tail of the last
+            // key tile, which without causal masking no step masks) get
+            // t = r = 0 here: their K rows load as zero, but their P would
+            // still enter the row masses rho and m.
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int mq = 0; mq < 2; ++mq) {
-                    bf16x4 w4;
+                    const uint64_t keep = k0w + 16 * kb + c16 < Nk ? ~0ull : 0ull;
+                    bf16x4 w4, r4;
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) w4[i] = tf[kb][4 * mq + i];
-                    *reinterpret_cast<bf16x4*>(
-                        Xt + tile_off<kTile>(32 * kh + 16 * kb + c16, 32 * qh + 16 * mq + 4 * g)) = w4;
+                    for (int i = 0; i < 4; ++i) {
+                        w4[i] = tf[kb][4 * mq + i];
+                        r4[i] = rf[kb][4 * mq + i];
+                    }
+                    const int xo = tile_off<kTile>(32 * kh + 16 * kb + c16, 32 * qh + 16 * mq + 4 * g);
+                    *reinterpret_cast<uint64_t*>(Xt + xo) = __builtin_bit_cast(uint64_t, w4) & keep;
+                    if (AB)
+                        *reinterpret_cast<uint64_t*>(Xr + xo) = __builtin_bit_cast(uint64_t, r4) & keep;
                 }
             __syncthreads();
-            // A block of this tile's share of A = tK: wave w takes queries
-            // 16 w .. 16 w + 15 against all 64 keys.  Operands: t[query][key]
-            // and K[key][d], both read transposed (key along k).
-            f32x4 aq[MB];
+            // A block of this tile's share of A = tK (and B = rK): wave w takes
+            // queries 16 w .. 16 w + 15 against all 64 keys.  Operands:
+            // t[query][key] and K[key][d], both read transposed (key along k).
+            // rho and m: the same t, r operands against a B operand whose
+            // column 0 is ones, so accumulator column 0 holds the row sums.
+            f32x4 aq[MB], bq[AB ? MB : 1], rsum = {0.f, 0.f, 0.f, 0.f}, msum = rsum;
 #pragma unroll
             for (int db = 0; db < MB; ++db) aq[db] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
+            for (int db = 0; db < (AB ? MB : 1); ++db) bq[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
             for (int kc = 0; kc < 2; ++kc) {
                 const bf16x8 ta = ld_tr_operand<kTile>(Xt, 32 * kc, 16 * wave, c16, g);
+                bf16x8 ra = ta;
+                if (AB) ra = ld_tr_operand<kTile>(Xr, 32 * kc, 16 * wave, c16, g);
 #pragma unroll
-                for (int db = 0; db < MB; ++db)
-                    aq[db] = mfma_16x16x32(ta, ld_tr_operand<D>(Ks, 32 * kc, 16 * db, c16, g), aq[db]);
+                for (int db = 0; db < MB; ++db) {
+                    const bf16x8 kop = ld_tr_operand<D>(Ks, 32 * kc, 16 * db, c16, g);
+                    aq[db] = mfma_16x16x32(ta, kop, aq[db]);
+                    if (AB) bq[db] = mfma_16x16x32(ra, kop, bq[db]);
+                }
+                if (AB) {
+                    const bf16x8 ones = ones_row0(c16);
+                    rsum = mfma_16x16x32(ta, ones, rsum);
+                    msum = mfma_16x16x32(ra, ones, msum);
+                }
             }
             // FP32 atomic adds through a buffer resource over this head's N
             // rows (rows beyond N are dropped by the range check): lanes c16
@@ -666,11 +704,23 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
             // bytes per row and instruction.
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const uint32_t off = (uint32_t)((q0 + 16 * wave + 4 * g + i) * D + c16) * 4u;
+                const int qr = q0 + 16 * wave + 4 * g + i;
+                const uint32_t off = (uint32_t)(qr * D + c16) * 4u;
 #pragma unroll
-                for (int db = 0; db < MB; ++db)
+                for (int db = 0; db < MB; ++db) {
                     __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(aq[db][i], rdq, off + 64u * db, 0,
                                                                     0);
+                    if (AB)
+                        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(bq[db][i], rdb,
+                                                                        off + 64u * db, 0, 0);
+                }
+                // the row sums sit in accumulator column 0 (lanes c16 == 0)
+                if (AB && c16 == 0) {
+                    __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(rsum[i], rrho, (uint32_t)qr * 4u, 0,
+                                                                    0);
+                    __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(msum[i], rms, (uint32_t)qr * 4u, 0,
+                                                                    0);
+                }
             }
             // The atomics share the vector-memory counter with the tile
             // fills; wait for everything rather than rely on the order in
@@ -739,6 +789,25 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
             }
             continue;
         }
+        if (AB && dKacc != nullptr) {
+            // the FP32 dK^acc for the correction pass, unscaled; dV final
+            float* kp = dKacc + kvoff + (size_t)krow * D;
+            uint16_t* vrow = dV + kvoff + (size_t)krow * D;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+                f32x4 dk;
+                float dv[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int j = (mb * 4 + i) * NV;
+                    dv[i] = red[kb][j];
+                    dk[i] = red[kb][j + 1];
+                }
+                *reinterpret_cast<f32x4*>(kp + mb * 16 + 4 * g) = dk;
+                st_bf16x4(vrow + mb * 16 + 4 * g, dv[0], dv[1], dv[2], dv[3]);
+            }
+            continue;
+        }
         uint16_t* vrow = dV + kvoff + (size_t)krow * D;
         uint16_t* krw = dK + kvoff + (size_t)krow * D;
 #pragma unroll
@@ -752,6 +821,164 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
                 dk[i] = scale * red[kb][j + 1];
             }
             st_bf16x4(vrow + mb * 16 + 4 * g, dv[0], dv[1], dv[2], dv[3]);
+            st_bf16x4(krw + mb * 16 + 4 * g, dk[0], dk[1], dk[2], dk[3]);
+        }
+    }
+}
+
+// Second key-major pass of the atomic GProj schedule (Algorithm 1's loop for
+// the key correction; eq. gproj-key-implemented), dense multi-head.  With
+// lambda known, it rebuilds P and r-tilde for every causal pair with the first
+// pass's instructions (so r-tilde = r bitwise), accumulates -C = r^T (-z) in
+// FP32 over the query tiles and writes
+// dK = BF16(fl32[alpha fl32(dK^acc - C)]) from the first pass's FP32 dK^acc.
+// Same work split, ring and statistics staging as bwd_dkdv_kernel, with two
+// staged tensors (Q for the logits, -z for the product) and no dP.
+template <int D>
+__global__ __launch_bounds__(kThreads, D == 64 ? 2 : 1) void bwd_dk_corr_kernel(
+    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
+    const float* __restrict__ TS, const uint16_t* __restrict__ Z,
+    const float* __restrict__ dKacc, uint16_t* __restrict__ dK, int BH, int N, int causal,
+    float scale) {
+    constexpr int MB = D / 16;
+    constexpr int KC = D / 32;
+    constexpr int NT = 2;
+    constexpr int TILE_E = kTile * D;
+    constexpr int STAT_E = kWaves * 128;
+    constexpr int SLOT_E = NT * TILE_E + STAT_E;
+    __shared__ __attribute__((aligned(16))) uint16_t B0[SLOT_E];
+    __shared__ __attribute__((aligned(16))) uint16_t B1[SLOT_E];
+    __shared__ __attribute__((aligned(16))) uint16_t B2[SLOT_E];
+
+    const int T = (N + kTile - 1) / kTile;
+    int bh, tile;
+    map_block(blockIdx.x, BH, T, false, &bh, &tile);
+    const size_t hoff = (size_t)bh * N * D;
+    const float* tsh = TS + (size_t)bh * T * kStatFloats;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, c16 = lane & 15;
+    const int kh = wave & 1;
+    const int qh = wave >> 1;
+    const int k0w = tile * kTile + 32 * kh;
+
+    const rsrc_t rk = make_rsrc(K + hoff, (uint32_t)N * (2 * D));
+    bf16x8 kf[2][KC];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int kc = 0; kc < KC; ++kc)
+            kf[kb][kc] = __builtin_bit_cast(
+                bf16x8, ld_row16<D>(rk, k0w + kb * 16 + c16, kc * 32 + 8 * g));
+    const float c = scale * kLog2e;
+    f32x4 accC[2][MB];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) accC[kb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // dense rows: a query tile below this key tile sees none of its keys
+    const int qt0 = causal ? tile : 0;
+    const int moff = causal ? 0 : (1 << 30);
+    const uint16_t* src[NT] = {Q + hoff, Z + hoff};
+    TileDma<D> dma;
+    dma.init(lane, wave);
+    constexpr int FILL_VM = NT * TileDma<D>::CALLS + 1;
+    auto fill = [&](uint16_t* slot, int qt) {
+        const bool valid = qt < T;
+        stat_dma(tsh + (size_t)(valid ? qt : 0) * kStatFloats,
+                 reinterpret_cast<float*>(slot + NT * TILE_E) + 64 * wave, lane, qh, valid);
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+            for (int k = 0; k < TileDma<D>::CALLS; ++k)
+                dma.load_call(src[t], slot + t * TILE_E, qt * kTile, N, valid, k);
+    };
+    wait_vm_lgkm0<0>();
+    fill(B0, qt0);
+    fill(B1, qt0 + 1);
+    wait_vm_lgkm0<FILL_VM>();
+    __builtin_amdgcn_s_barrier();
+
+    auto step = [&](auto masked, int qt, const uint16_t* cur, uint16_t* nxt2) {
+        constexpr bool MASK = decltype(masked)::value;
+        const int q0 = qt * kTile;
+        fill(nxt2, qt + 2);
+        const uint16_t* Qc = cur;
+        const uint16_t* Zc = cur + TILE_E;
+        const float* st = reinterpret_cast<const float*>(cur + NT * TILE_E) + 64 * wave;
+        f32x4 l2[2];
+#pragma unroll
+        for (int mq = 0; mq < 2; ++mq) l2[mq] = *reinterpret_cast<const f32x4*>(st + mq * 16 + 4 * g);
+        const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+        bf16x8 tf[2], rf[2];
+#pragma unroll
+        for (int mq = 0; mq < 2; ++mq) {
+            const int row = 32 * qh + mq * 16 + c16;
+            bf16x8 qa[KC];
+#pragma unroll
+            for (int kc = 0; kc < KC; ++kc) qa[kc] = ld_b128(Qc + tile_off<D>(row, kc * 32 + 8 * g));
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+                f32x4 sv = zero4;
+#pragma unroll
+                for (int kc = 0; kc < KC; ++kc) sv = mfma_16x16x32(qa[kc], kf[kb][kc], sv);
+                // the first pass's probability code; t is not used here
+                dkdv_probs<MASK>(sv, zero4, l2[mq], zero4, c, q0 + 32 * qh + mq * 16, g,
+                                 k0w + kb * 16 + c16, moff, mq, tf[kb], rf[kb]);
+            }
+        }
+        // -C^T[d][key] += (-z)^T r
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            const bf16x8 za = ld_tr_operand<D>(Zc, 32 * qh, mb * 16, c16, g);
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) accC[kb][mb] = mfma_16x16x32(za, rf[kb], accC[kb][mb]);
+        }
+        wait_vm_lgkm0<FILL_VM>();
+        __builtin_amdgcn_s_barrier();
+    };
+    const std::false_type plain;
+    const std::true_type masked;
+    if (qt0 < T) step(masked, qt0, B0, B2);
+    if (qt0 + 1 < T) step(masked, qt0 + 1, B1, B0);
+    for (int qt = qt0 + 2; qt < T; qt += 3) {
+        step(plain, qt, B2, B1);
+        if (qt + 1 < T) step(plain, qt + 1, B0, B2);
+        if (qt + 2 < T) step(plain, qt + 2, B1, B0);
+    }
+    wait_vm_lgkm0<0>();
+    __builtin_amdgcn_s_barrier();
+
+    constexpr int PER_KB = MB * 4;
+    float red[2][PER_KB];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) red[kb][mb * 4 + i] = accC[kb][mb][i];
+        if (kb) __syncthreads();
+        pair_reduce<PER_KB, sizeof(B0) / 4>(red[kb], reinterpret_cast<float*>(B0), wave, lane);
+    }
+    if (wave >= 2) return;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+        const int krow = k0w + kb * 16 + c16;
+        if (krow >= N) continue;
+        const float* ka = dKacc + hoff + (size_t)krow * D;
+        uint16_t* krw = dK + hoff + (size_t)krow * D;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+            const f32x4 a = *reinterpret_cast<const f32x4*>(ka + mb * 16 + 4 * g);
+            float dk[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+#pragma clang fp contract(off)
+                const float diff = a[i] + red[kb][mb * 4 + i];  // dK^acc - C (-C accumulated)
+                dk[i] = scale * diff;
+            }
             st_bf16x4(krw + mb * 16 + 4 * g, dk[0], dk[1], dk[2], dk[3]);
         }
     }
@@ -786,17 +1013,21 @@ __global__ __launch_bounds__(256) void group_sum_kernel(const float* __restrict_
     st_bf16x4(dV + kvh * per_head + e, sv[0], sv[1], sv[2], sv[3]);
 }
 
-// Preprocessing of the fused plain pass (dense multi-head): Algorithm 1's
+// Preprocessing of the atomic schedule (dense multi-head): Algorithm 1's
 // D_i = sum_c fl32(dO_ic O_ic) with the query-major pass's own lanes and
 // summation order (so its bits, and hence t, equal that pass's), the per-tile
-// statistics block the key-major pass stages, and a zeroed dQ accumulator.
+// statistics block the key-major pass stages, and zeroed accumulators: A
+// (dQacc) always, B, rho and m when given (the GProj modes).
 // One workgroup per (head, 64-row tile); wave w takes rows 16 w .. 16 w + 15.
 template <int D>
 __global__ __launch_bounds__(kThreads) void bwd_pre_kernel(const uint16_t* __restrict__ O,
                                                            const uint16_t* __restrict__ dO,
                                                            const float* __restrict__ LSE,
                                                            float* __restrict__ TS,
-                                                           float* __restrict__ dQacc, int BH,
+                                                           float* __restrict__ dQacc,
+                                                           float* __restrict__ Bacc,
+                                                           float* __restrict__ rho_acc,
+                                                           float* __restrict__ m_acc, int BH,
                                                            int N) {
     constexpr int KC = D / 32;
     const int T = (N + kTile - 1) / kTile;
@@ -830,7 +1061,60 @@ __global__ __launch_bounds__(kThreads) void bwd_pre_kernel(const uint16_t* __res
 #pragma unroll
         for (int c = 0; c < D / 4; c += 4)
             *reinterpret_cast<f32x4*>(a + 4 * (c + g)) = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (Bacc != nullptr) {
+            float* b = Bacc + hoff + (size_t)qrow * D;
+#pragma unroll
+            for (int c = 0; c < D / 4; c += 4)
+                *reinterpret_cast<f32x4*>(b + 4 * (c + g)) = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (g == 0) {
+                rho_acc[(size_t)bh * N + qrow] = 0.f;
+                m_acc[(size_t)bh * N + qrow] = 0.f;
+            }
+        }
     }
+}
+
+// The atomic schedule's lambda and dQ (eq. gproj-query-implemented): per row
+// lambda = rho / m (one IEEE FP32 division, 0 where m = 0) and
+// dQ = BF16(fl32[alpha fl32(A - fl32(lambda B))]) from the FP32 accumulators;
+// with Zneg also -z = BF16(fl32(-lambda q)) for the correction pass, and with
+// lam_out lambda itself.  Thread t takes 8 consecutive elements of one row.
+template <int D>
+__global__ __launch_bounds__(256) void bwd_gproj_finalize_kernel(
+    const float* __restrict__ A, const float* __restrict__ Bm, const float* __restrict__ rho,
+    const float* __restrict__ msum, const uint16_t* __restrict__ Q, uint16_t* __restrict__ dQ,
+    uint16_t* __restrict__ Zneg, float* __restrict__ lam_out, size_t rows, float scale) {
+    constexpr int PER = D / 8;
+    const size_t t = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= rows * PER) return;
+    const size_t row = t / PER;
+    const int part = (int)(t - row * PER);
+    const size_t e = row * D + 8 * part;
+    const float m = msum[row];
+    const float lam = (m != 0.f) ? rho[row] / m : 0.f;  // one IEEE FP32 division
+    float v[8];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const f32x4 a = *reinterpret_cast<const f32x4*>(A + e + 4 * h);
+        const f32x4 b = *reinterpret_cast<const f32x4*>(Bm + e + 4 * h);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+#pragma clang fp contract(off)
+            const float corr = lam * b[i];
+            const float diff = a[i] - corr;
+            v[4 * h + i] = scale * diff;
+        }
+    }
+    st_bf16x4(dQ + e, v[0], v[1], v[2], v[3]);
+    st_bf16x4(dQ + e + 4, v[4], v[5], v[6], v[7]);
+    if (Zneg != nullptr) {
+        const bf16x8 q = *reinterpret_cast<const bf16x8*>(Q + e);
+        bf16x8 z;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) z[i] = to_bf16(-lam * bf16_to_f32(q[i]));
+        *reinterpret_cast<bf16x8*>(Zneg + e) = z;
+    }
+    if (lam_out != nullptr && part == 0) lam_out[row] = lam;
 }
 
 // dQ = BF16(fl32(alpha A)) from the FP32 accumulator, 4 elements per thread.
@@ -852,29 +1136,62 @@ __global__ __launch_bounds__(256) void bwd_dq_finalize_kernel(const float* __res
 }  // namespace
 
 hipError_t launch_bwd_pre(const uint16_t* O, const uint16_t* dO, const float* LSE, float* TS,
-                          float* dQacc, const Shape& s, hipStream_t st) {
+                          const AtomicAcc& a, const Shape& s, hipStream_t st) {
     const int T = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
     if (s.d == 64)
-        bwd_pre_kernel<64><<<grid, block, 0, st>>>(O, dO, LSE, TS, dQacc, s.BH, s.N);
+        bwd_pre_kernel<64><<<grid, block, 0, st>>>(O, dO, LSE, TS, a.A, a.B, a.rho, a.m, s.BH,
+                                                   s.N);
     else
-        bwd_pre_kernel<128><<<grid, block, 0, st>>>(O, dO, LSE, TS, dQacc, s.BH, s.N);
+        bwd_pre_kernel<128><<<grid, block, 0, st>>>(O, dO, LSE, TS, a.A, a.B, a.rho, a.m, s.BH,
+                                                    s.N);
     return hipGetLastError();
 }
 
-hipError_t launch_bwd_fused_plain(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                                  const uint16_t* dO, const float* TS, uint16_t* dK, uint16_t* dV,
-                                  float* dQacc, const Shape& s, hipStream_t st) {
+hipError_t launch_bwd_fused(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                            const uint16_t* dO, const float* TS, uint16_t* dK, uint16_t* dV,
+                            const AtomicAcc& a, int mode, const Shape& s, hipStream_t st) {
+    const int Tk = (s.N + kTile - 1) / kTile;
+    dim3 grid((unsigned)(s.BH * Tk)), block(kThreads);
+    float* dKacc = mode == 2 ? a.dKacc : nullptr;
+#define GPA_FUSED(DD, GP)                                                                    \
+    bwd_dkdv_kernel<DD, GP, true><<<grid, block, 0, st>>>(                                   \
+        Q, K, V, dO, TS, nullptr, dK, dV, nullptr, nullptr, s.BH, s.N, s.causal, s.scale, 1, \
+        nullptr, s.BH, 0, nullptr, 0, s.N, a.A, a.B, a.rho, a.m, dKacc)
+    if (s.d == 64) {
+        if (mode == 0) GPA_FUSED(64, false); else GPA_FUSED(64, true);
+    } else {
+        if (mode == 0) GPA_FUSED(128, false); else GPA_FUSED(128, true);
+    }
+#undef GPA_FUSED
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_gproj_finalize(const AtomicAcc& a, const uint16_t* Q, uint16_t* dQ,
+                                     uint16_t* Zneg, float* lam, const Shape& s, hipStream_t st) {
+    const size_t rows = (size_t)s.BH * s.N;
+    const size_t threads = rows * (size_t)(s.d / 8);
+    dim3 grid((unsigned)((threads + 255) / 256)), block(256);
+    if (s.d == 64)
+        bwd_gproj_finalize_kernel<64><<<grid, block, 0, st>>>(a.A, a.B, a.rho, a.m, Q, dQ, Zneg,
+                                                              lam, rows, s.scale);
+    else
+        bwd_gproj_finalize_kernel<128><<<grid, block, 0, st>>>(a.A, a.B, a.rho, a.m, Q, dQ, Zneg,
+                                                               lam, rows, s.scale);
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_dk_corr(const uint16_t* Q, const uint16_t* K, const float* TS,
+                              const uint16_t* Zneg, const float* dKacc, uint16_t* dK,
+                              const Shape& s, hipStream_t st) {
     const int Tk = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * Tk)), block(kThreads);
     if (s.d == 64)
-        bwd_dkdv_kernel<64, false, true><<<grid, block, 0, st>>>(
-            Q, K, V, dO, TS, nullptr, dK, dV, nullptr, nullptr, s.BH, s.N, s.causal, s.scale, 1,
-            nullptr, s.BH, 0, nullptr, 0, s.N, dQacc);
+        bwd_dk_corr_kernel<64><<<grid, block, 0, st>>>(Q, K, TS, Zneg, dKacc, dK, s.BH, s.N,
+                                                       s.causal, s.scale);
     else
-        bwd_dkdv_kernel<128, false, true><<<grid, block, 0, st>>>(
-            Q, K, V, dO, TS, nullptr, dK, dV, nullptr, nullptr, s.BH, s.N, s.causal, s.scale, 1,
-            nullptr, s.BH, 0, nullptr, 0, s.N, dQacc);
+        bwd_dk_corr_kernel<128><<<grid, block, 0, st>>>(Q, K, TS, Zneg, dKacc, dK, s.BH, s.N,
+                                                        s.causal, s.scale);
     return hipGetLastError();
 }
 

@@ -40,7 +40,8 @@ enum KernelId {
     kKBwdPre = 7,
     kKBwdFused = 8,
     kKBwdFinal = 9,
-    kNumKernels = 10
+    kKBwdCorr = 10,
+    kNumKernels = 11
 };
 
 // fma_forward selects the historical exponent rounding (diagnostic only).
@@ -66,19 +67,38 @@ hipError_t launch_bwd_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t*
                            uint16_t* dK, uint16_t* dV, float* dKp, float* dVp, int mode,
                            const Shape& s, hipStream_t st);
 
-// Single key-major plain backward with FP32 atomic dQ (dense multi-head):
-// launch_bwd_pre writes the per-tile statistics TS ([BH, T, 2, 64], as the
-// query-major pass does, same D bits) and zeroes dQacc ([BH, N, d] FP32);
-// launch_bwd_fused_plain writes dK, dV (the plain key pass's arithmetic) and
-// adds t K into dQacc with atomics; launch_bwd_dq_finalize writes
-// dQ = BF16(scale * dQacc).
+// FP32 accumulators of the atomic schedule ([BH, N, d] for A, B and dK^acc,
+// [BH, N] for rho and m); B, rho, m are null in plain mode, dKacc outside
+// gproj mode.
+struct AtomicAcc {
+    float* A = nullptr;
+    float* B = nullptr;
+    float* rho = nullptr;
+    float* m = nullptr;
+    float* dKacc = nullptr;
+};
+
+// Algorithm 1's schedule with atomics (dense multi-head): launch_bwd_pre
+// writes the per-tile statistics TS ([BH, T, 2, 64], as the query-major pass
+// does, same D bits) and zeroes the accumulators; launch_bwd_fused runs the
+// single key-major pass: dV, and dK (plain, gproj_q: the plain key pass's
+// arithmetic) or the FP32 dK^acc (gproj), with t K (and in the GProj modes
+// r K, rho, m) added by atomics; launch_bwd_dq_finalize writes
+// dQ = BF16(scale * A) (plain); launch_bwd_gproj_finalize forms lambda, dQ
+// and, with Zneg, -z = BF16(-lambda Q); launch_bwd_dk_corr is the gproj
+// correction pass that writes dK.
 hipError_t launch_bwd_pre(const uint16_t* O, const uint16_t* dO, const float* LSE, float* TS,
-                          float* dQacc, const Shape& s, hipStream_t st);
-hipError_t launch_bwd_fused_plain(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
-                                  const uint16_t* dO, const float* TS, uint16_t* dK, uint16_t* dV,
-                                  float* dQacc, const Shape& s, hipStream_t st);
+                          const AtomicAcc& a, const Shape& s, hipStream_t st);
+hipError_t launch_bwd_fused(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                            const uint16_t* dO, const float* TS, uint16_t* dK, uint16_t* dV,
+                            const AtomicAcc& a, int mode, const Shape& s, hipStream_t st);
 hipError_t launch_bwd_dq_finalize(const float* dQacc, uint16_t* dQ, const Shape& s,
                                   hipStream_t st);
+hipError_t launch_bwd_gproj_finalize(const AtomicAcc& a, const uint16_t* Q, uint16_t* dQ,
+                                     uint16_t* Zneg, float* lam, const Shape& s, hipStream_t st);
+hipError_t launch_bwd_dk_corr(const uint16_t* Q, const uint16_t* K, const float* TS,
+                              const uint16_t* Zneg, const float* dKacc, uint16_t* dK,
+                              const Shape& s, hipStream_t st);
 
 // dK = BF16(scale * sum_g dKp), dV = BF16(sum_g dVp) over the G query heads of
 // each key/value head, in head order.

@@ -94,6 +94,28 @@ def test_bwd_validation(lib):
     assert _bwd(lib, d=80) == 2
 
 
+def test_atomic_schedule_workspace_and_validation(lib):
+    import paper_2609_34272_amd as gpa
+    B, H, N, d = 1, 16, 4096, 64
+    big = B * H * N * d * 4
+    plain = gpa.attn_bwd_atomic_workspace_bytes(B, H, N, d, "plain")
+    gq = gpa.attn_bwd_atomic_workspace_bytes(B, H, N, d, "gproj_q")
+    gp = gpa.attn_bwd_atomic_workspace_bytes(B, H, N, d, "gproj")
+    # A; then B, rho, m; then dK^acc (FP32) and -z (BF16)
+    assert plain >= big
+    assert gq - plain >= big + 2 * B * H * N * 4
+    assert gp - gq >= big + big // 2
+    assert all(v % 256 == 0 for v in (plain, gq, gp))
+    assert lib.gpa_attn_bwd_atomic_workspace_bytes(1, 1, 8, 64, 3) == 0
+    assert lib.gpa_attn_bwd_atomic_workspace_bytes(1, 1, 8, 80, 0) == 0
+    args = [FAKE + i * 0x10000000 for i in range(9)]
+    ws = FAKE + 0x90000000
+    need = lib.gpa_attn_bwd_atomic_workspace_bytes(1, 1, 128, 64, 2)
+    assert lib.gpa_attn_bwd_atomic(*args, 1, 1, 128, 64, 1, 0.125, 3, ws, need, None) == 1
+    assert lib.gpa_attn_bwd_atomic(*args, 1, 1, 128, 64, 1, 0.125, 2, ws, need - 256, None) == 3
+    assert lib.gpa_attn_bwd_atomic(*args, 1, 1, 128, 64, 1, 0.125, 2, None, need, None) == 3
+
+
 def test_fp32_validation(lib):
     args = [FAKE + i * 0x10000000 for i in range(9)]
     assert lib.gpa_fp32_attn(*args, 1, 1, 64, 64, 1, 0.125, None, 0, None) == 3
