@@ -279,7 +279,8 @@ def main():
     wall = time.perf_counter() - t_wall0
     value = flops / (ms * 1e-3) / 1e12
 
-    # Per-kernel durations (HIP events recorded by the library on the launch stream).
+    # Per-kernel durations (HIP events that each kernel launch records at the
+    # kernel's start and end on its stream).
     gpa.profile_enable(True)
     for _ in range(args.steps):
         step(args.mode)

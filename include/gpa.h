@@ -321,7 +321,8 @@ gpa_status gpa_fp32_attn(const uint16_t* Q, const uint16_t* K, const uint16_t* V
 
 /*
  * Kernel timing for measurement.  While enabled, every kernel the library
- * launches is bracketed by HIP events on its stream.  gpa_profile_read
+ * launches records a pair of HIP events at its own start and end on its
+ * stream (hipExtLaunchKernel's start and stop events).  gpa_profile_read
  * synchronises those events, writes per-kernel totals (milliseconds) and launch
  * counts for kernel ids 0..n-1 (see gpa_kernel_name), clears them, and
  * returns the number of ids.  Not thread-safe; meant for benchmarks.

@@ -13,6 +13,15 @@
 #include "gpa.h"
 #include "gpa_launch.h"
 
+namespace gpa {
+
+LaunchEvents& launch_events() {
+    static thread_local LaunchEvents e;
+    return e;
+}
+
+}  // namespace gpa
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -93,13 +102,16 @@ hipEvent_t take_event() {
     return e;
 }
 
+// With timing on, the launcher's kernel records the pair of events at its own
+// start and end (launch_kernel), so each record is one kernel's duration.
 template <class F>
 hipError_t timed(int id, hipStream_t st, F&& launch) {
+    (void)st;
     if (!g_prof) return launch();
     hipEvent_t a = take_event(), b = take_event();
-    if (a) (void)hipEventRecord(a, st);
+    gpa::launch_events() = {a, b};
     const hipError_t e = launch();
-    if (b) (void)hipEventRecord(b, st);
+    gpa::launch_events() = {};
     if (a && b) g_recs.push_back({id, a, b});
     return e;
 }

@@ -1140,11 +1140,11 @@ hipError_t launch_bwd_pre(const uint16_t* O, const uint16_t* dO, const float* LS
     const int T = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
     if (s.d == 64)
-        bwd_pre_kernel<64><<<grid, block, 0, st>>>(O, dO, LSE, TS, a.A, a.B, a.rho, a.m, s.BH,
-                                                   s.N);
+        launch_kernel(bwd_pre_kernel<64>, grid, block, st, O, dO, LSE, TS, a.A, a.B, a.rho, a.m,
+                      s.BH, s.N);
     else
-        bwd_pre_kernel<128><<<grid, block, 0, st>>>(O, dO, LSE, TS, a.A, a.B, a.rho, a.m, s.BH,
-                                                    s.N);
+        launch_kernel(bwd_pre_kernel<128>, grid, block, st, O, dO, LSE, TS, a.A, a.B, a.rho, a.m,
+                      s.BH, s.N);
     return hipGetLastError();
 }
 
@@ -1155,9 +1155,9 @@ hipError_t launch_bwd_fused(const uint16_t* Q, const uint16_t* K, const uint16_t
     dim3 grid((unsigned)(s.BH * Tk)), block(kThreads);
     float* dKacc = mode == 2 ? a.dKacc : nullptr;
 #define GPA_FUSED(DD, GP)                                                                    \
-    bwd_dkdv_kernel<DD, GP, true><<<grid, block, 0, st>>>(                                   \
-        Q, K, V, dO, TS, nullptr, dK, dV, nullptr, nullptr, s.BH, s.N, s.causal, s.scale, 1, \
-        nullptr, s.BH, 0, nullptr, 0, s.N, a.A, a.B, a.rho, a.m, dKacc)
+    launch_kernel(bwd_dkdv_kernel<DD, GP, true>, grid, block, st, Q, K, V, dO, TS, nullptr,  \
+                  dK, dV, nullptr, nullptr, s.BH, s.N, s.causal, s.scale, 1, nullptr, s.BH, 0, \
+                  nullptr, 0, s.N, a.A, a.B, a.rho, a.m, dKacc)
     if (s.d == 64) {
         if (mode == 0) GPA_FUSED(64, false); else GPA_FUSED(64, true);
     } else {
@@ -1173,11 +1173,11 @@ hipError_t launch_bwd_gproj_finalize(const AtomicAcc& a, const uint16_t* Q, uint
     const size_t threads = rows * (size_t)(s.d / 8);
     dim3 grid((unsigned)((threads + 255) / 256)), block(256);
     if (s.d == 64)
-        bwd_gproj_finalize_kernel<64><<<grid, block, 0, st>>>(a.A, a.B, a.rho, a.m, Q, dQ, Zneg,
-                                                              lam, rows, s.scale);
+        launch_kernel(bwd_gproj_finalize_kernel<64>, grid, block, st, a.A, a.B, a.rho, a.m, Q,
+                      dQ, Zneg, lam, rows, s.scale);
     else
-        bwd_gproj_finalize_kernel<128><<<grid, block, 0, st>>>(a.A, a.B, a.rho, a.m, Q, dQ, Zneg,
-                                                               lam, rows, s.scale);
+        launch_kernel(bwd_gproj_finalize_kernel<128>, grid, block, st, a.A, a.B, a.rho, a.m, Q,
+                      dQ, Zneg, lam, rows, s.scale);
     return hipGetLastError();
 }
 
@@ -1187,11 +1187,11 @@ hipError_t launch_bwd_dk_corr(const uint16_t* Q, const uint16_t* K, const float*
     const int Tk = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * Tk)), block(kThreads);
     if (s.d == 64)
-        bwd_dk_corr_kernel<64><<<grid, block, 0, st>>>(Q, K, TS, Zneg, dKacc, dK, s.BH, s.N,
-                                                       s.causal, s.scale);
+        launch_kernel(bwd_dk_corr_kernel<64>, grid, block, st, Q, K, TS, Zneg, dKacc, dK, s.BH,
+                      s.N, s.causal, s.scale);
     else
-        bwd_dk_corr_kernel<128><<<grid, block, 0, st>>>(Q, K, TS, Zneg, dKacc, dK, s.BH, s.N,
-                                                        s.causal, s.scale);
+        launch_kernel(bwd_dk_corr_kernel<128>, grid, block, st, Q, K, TS, Zneg, dKacc, dK, s.BH,
+                      s.N, s.causal, s.scale);
     return hipGetLastError();
 }
 
@@ -1199,7 +1199,7 @@ hipError_t launch_bwd_dq_finalize(const float* dQacc, uint16_t* dQ, const Shape&
                                   hipStream_t st) {
     const size_t quads = (size_t)s.BH * s.N * s.d / 4;
     dim3 grid((unsigned)((quads + 255) / 256)), block(256);
-    bwd_dq_finalize_kernel<<<grid, block, 0, st>>>(dQacc, dQ, quads, s.scale);
+    launch_kernel(bwd_dq_finalize_kernel, grid, block, st, dQacc, dQ, quads, s.scale);
     return hipGetLastError();
 }
 
@@ -1211,10 +1211,9 @@ hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V
     const int Nk = s.Nk > 0 ? s.Nk : s.N;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
 #define GPA_DQ(DD, GP, WZ)                                                                   \
-    bwd_dq_kernel<DD, GP, WZ><<<grid, block, 0, st>>>(Q, K, V, O, dO, LSE, Drow, TS, dQ, rho, \
-                                                      msum, lambda, Z, s.BH, s.N, s.causal,  \
-                                                      s.scale, s.G, s.cu, s.Hq, s.total,     \
-                                                      s.cu_k, s.total_k, Nk)
+    launch_kernel(bwd_dq_kernel<DD, GP, WZ>, grid, block, st, Q, K, V, O, dO, LSE, Drow, TS, \
+                  dQ, rho, msum, lambda, Z, s.BH, s.N, s.causal, s.scale, s.G, s.cu, s.Hq,   \
+                  s.total, s.cu_k, s.total_k, Nk)
     if (s.d == 64) {
         if (mode == 2) GPA_DQ(64, true, true);
         else if (mode == 1) GPA_DQ(64, true, false);
@@ -1236,10 +1235,10 @@ hipError_t launch_bwd_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t*
     const int Tk = (Nk + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * Tk)), block(kThreads);
     const bool gp = mode == 2;
-#define GPA_DKDV(DD, GP)                                                             \
-    bwd_dkdv_kernel<DD, GP><<<grid, block, 0, st>>>(Q, K, V, dO, TS, Z, dK, dV, dKp, dVp, \
-                                                    s.BH, s.N, s.causal, s.scale, s.G, s.cu, \
-                                                    s.Hq, s.total, s.cu_k, s.total_k, Nk)
+#define GPA_DKDV(DD, GP)                                                                      \
+    launch_kernel(bwd_dkdv_kernel<DD, GP>, grid, block, st, Q, K, V, dO, TS, Z, dK, dV, dKp, \
+                  dVp, s.BH, s.N, s.causal, s.scale, s.G, s.cu, s.Hq, s.total, s.cu_k,       \
+                  s.total_k, Nk, nullptr, nullptr, nullptr, nullptr, nullptr)
     if (s.d == 64) {
         if (gp) GPA_DKDV(64, true); else GPA_DKDV(64, false);
     } else {
@@ -1255,7 +1254,7 @@ hipError_t launch_bwd_group_sum(const float* dKp, const float* dVp, uint16_t* dK
     const size_t per_head = (size_t)s.N * s.d;
     const size_t threads = (size_t)BHkv * (per_head / 4);
     dim3 grid((unsigned)((threads + 255) / 256)), block(256);
-    group_sum_kernel<<<grid, block, 0, st>>>(dKp, dVp, dK, dV, BHkv, s.G, per_head, s.scale);
+    launch_kernel(group_sum_kernel, grid, block, st, dKp, dVp, dK, dV, BHkv, s.G, per_head, s.scale);
     return hipGetLastError();
 }
 

@@ -467,11 +467,11 @@ hipError_t launch_f32_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* 
     const int T = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
     if (s.d == 64)
-        f32_fwd_kernel<64><<<grid, block, 0, st>>>(Q, K, V, O32, O, LSE, Mrow, Linv, s.BH, s.N,
-                                                   s.causal, s.scale);
+        launch_kernel(f32_fwd_kernel<64>, grid, block, st, Q, K, V, O32, O, LSE, Mrow, Linv, s.BH,
+                      s.N, s.causal, s.scale);
     else
-        f32_fwd_kernel<128><<<grid, block, 0, st>>>(Q, K, V, O32, O, LSE, Mrow, Linv, s.BH, s.N,
-                                                    s.causal, s.scale);
+        launch_kernel(f32_fwd_kernel<128>, grid, block, st, Q, K, V, O32, O, LSE, Mrow, Linv, s.BH,
+                      s.N, s.causal, s.scale);
     return hipGetLastError();
 }
 
@@ -482,11 +482,11 @@ hipError_t launch_f32_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V
     const int T = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
     if (s.d == 64)
-        f32_dq_kernel<64><<<grid, block, 0, st>>>(Q, K, V, dO, O32, Mrow, Linv, TS, dQ, s.BH, s.N,
-                                                  s.causal, s.scale);
+        launch_kernel(f32_dq_kernel<64>, grid, block, st, Q, K, V, dO, O32, Mrow, Linv, TS, dQ,
+                      s.BH, s.N, s.causal, s.scale);
     else
-        f32_dq_kernel<128><<<grid, block, 0, st>>>(Q, K, V, dO, O32, Mrow, Linv, TS, dQ, s.BH,
-                                                   s.N, s.causal, s.scale);
+        launch_kernel(f32_dq_kernel<128>, grid, block, st, Q, K, V, dO, O32, Mrow, Linv, TS, dQ,
+                      s.BH, s.N, s.causal, s.scale);
     return hipGetLastError();
 }
 
@@ -496,11 +496,11 @@ hipError_t launch_f32_dkdv(const uint16_t* Q, const uint16_t* K, const uint16_t*
     const int T = (s.N + kTile - 1) / kTile;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
     if (s.d == 64)
-        f32_dkdv_kernel<64><<<grid, block, 0, st>>>(Q, K, V, dO, TS, dK, dV, s.BH, s.N, s.causal,
-                                                    s.scale);
+        launch_kernel(f32_dkdv_kernel<64>, grid, block, st, Q, K, V, dO, TS, dK, dV, s.BH, s.N,
+                      s.causal, s.scale);
     else
-        f32_dkdv_kernel<128><<<grid, block, 0, st>>>(Q, K, V, dO, TS, dK, dV, s.BH, s.N, s.causal,
-                                                     s.scale);
+        launch_kernel(f32_dkdv_kernel<128>, grid, block, st, Q, K, V, dO, TS, dK, dV, s.BH, s.N,
+                      s.causal, s.scale);
     return hipGetLastError();
 }
 

@@ -446,9 +446,8 @@ hipError_t launch_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, u
     // d = 64: one 16-query block per wave (measured faster); d = 128: two
     // blocks per wave, whose halved LDS reads matter more there.
 #define GPA_FWD(KERNEL, DD, FM)                                                               \
-    KERNEL<DD, FM><<<grid, block, 0, st>>>(Q, K, V, O, LSE, s.BH, s.N, s.causal, s.scale, s.G, \
-                                           s.cu, s.Hq, s.total, s.cu_k, s.total_k,             \
-                                           s.Nk > 0 ? s.Nk : s.N)
+    launch_kernel(KERNEL<DD, FM>, grid, block, st, Q, K, V, O, LSE, s.BH, s.N, s.causal,      \
+                  s.scale, s.G, s.cu, s.Hq, s.total, s.cu_k, s.total_k, s.Nk > 0 ? s.Nk : s.N)
     if (s.d == 64) {
         if (fma_forward) GPA_FWD(fwd_sbs_q16_kernel, 64, true);
         else GPA_FWD(fwd_sbs_q16_kernel, 64, false);

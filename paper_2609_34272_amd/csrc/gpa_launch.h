@@ -2,10 +2,47 @@
 // include/gpa.h).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <tuple>
+
 namespace gpa {
+
+// Events of the launch being timed (both null unless the ABI layer's kernel
+// timing is on).  Per host thread.
+struct LaunchEvents {
+    hipEvent_t start = nullptr;
+    hipEvent_t stop = nullptr;
+};
+LaunchEvents& launch_events();
+
+// Launch `kernel` on `st` with the arguments converted to its parameter types
+// (their count must match).  While kernel timing is on, the launch goes
+// through hipExtLaunchKernel, which records the events when the kernel starts
+// and when it ends, so the elapsed time between them is the kernel's own
+// duration (events recorded around the launch would add the dispatch gap);
+// otherwise it is a plain hipLaunchKernel.  Errors are left for
+// hipGetLastError.
+template <typename... Formals, typename... Actuals>
+inline void launch_kernel(void (*kernel)(Formals...), dim3 grid, dim3 block, hipStream_t st,
+                          Actuals... actuals) {
+    static_assert(sizeof...(Formals) == sizeof...(Actuals), "kernel argument count");
+    std::tuple<Formals...> args{actuals...};
+    std::apply(
+        [&](auto&... a) {
+            void* ptrs[] = {static_cast<void*>(&a)...};
+            const LaunchEvents& e = launch_events();
+            if (e.start != nullptr || e.stop != nullptr)
+                (void)hipExtLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, ptrs,
+                                         0, st, e.start, e.stop, 0);
+            else
+                (void)hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, ptrs, 0,
+                                      st);
+        },
+        args);
+}
 
 struct Shape {
     int BH;        // batch * query heads (packed sequences: sequences * query heads)
