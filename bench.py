@@ -372,6 +372,14 @@ def main():
             for _ in range(3):
                 fn()
             gqa["bwd_ms"][m] = round(timed(fn, args.steps), 5)
+            if m == "gproj":
+                gpa.profile_enable(True)
+                for _ in range(args.steps):
+                    fn()
+                torch.cuda.synchronize()
+                gprof = gpa.profile_read()
+                gpa.profile_enable(False)
+                gqa["kernels_ms"] = {n: round(t / c, 5) for n, (t, c) in gprof.items() if c}
         gqa["gproj_bwd_overhead_vs_plain_pct"] = round(
             100.0 * (gqa["bwd_ms"]["gproj"] / gqa["bwd_ms"]["plain"] - 1), 2)
         del qg, kg, vg, ug, og, lg
@@ -461,6 +469,39 @@ def main():
     }
     if gqa is not None:
         out["gqa"] = gqa
+
+    # The memory-bound kernels against the HBM roofline: compulsory bytes per
+    # launch over the kernel's measured duration.  The group sum of the
+    # grouped-query backward, and the atomic schedule's preprocess and finalize
+    # kernels (the two-pass schedule folds those steps into its passes).
+    hbm = {}
+
+    def hbm_entry(name, ms_k, nbytes, what):
+        gbs = nbytes / (ms_k * 1e-3) / 1e9
+        hbm[name] = {"ms": round(ms_k, 5), "bytes": int(nbytes), "achieved_GB_s": round(gbs, 1),
+                     "peak_GB_s": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "bytes_counted": what}
+
+    ten = B * H * N * d                      # elements of one [B, H, N, d] tensor
+    rows = B * H * N
+    tile_stats = B * H * ((N + 63) // 64) * 128 * 4
+    ak = atomic_kern
+    hbm_entry("bwd_pre/plain", ak["plain"]["bwd_pre"], 2 * ten * 2 + rows * 4 + tile_stats + ten * 4,
+              "read O, dO, LSE; write the tile statistics; zero A")
+    hbm_entry("bwd_pre/gproj", ak["gproj"]["bwd_pre"],
+              2 * ten * 2 + rows * 4 + tile_stats + 2 * ten * 4 + 2 * rows * 4,
+              "read O, dO, LSE; write the tile statistics; zero A, B, rho, m")
+    hbm_entry("bwd_dq_finalize/plain", ak["plain"]["bwd_dq_finalize"], ten * 4 + ten * 2,
+              "read A; write dQ")
+    hbm_entry("bwd_gproj_finalize/gproj", ak["gproj"]["bwd_dq_finalize"],
+              2 * ten * 4 + 2 * rows * 4 + ten * 2 + 2 * ten * 2,
+              "read A, B, rho, m, Q; write dQ, -z")
+    if gqa is not None and "group_sum" in gqa.get("kernels_ms", {}):
+        wg = S.WORKLOADS[6]
+        hbm_entry("group_sum/" + wg.name + "/gproj", gqa["kernels_ms"]["group_sum"],
+                  2 * wg.B * wg.H * wg.N * wg.d * 4 + 2 * wg.B * wg.kv_heads * wg.N * wg.d * 2,
+                  "read the FP32 dK, dV contributions of every query head; write BF16 dK, dV")
+    out["hbm_bound_kernels"] = hbm
 
     # The wider-head, long-sequence and batched workloads, timed on the same
     # kernels (their parity is covered by the tests): forward and backward per

@@ -985,32 +985,61 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 2 : 1) void bwd_dk_corr_kernel(
 }
 
 // Group sum of the per-query-head FP32 contributions (G > 1): thread t of the
-// grid owns 4 consecutive elements of one key/value head and adds the G query
-// heads' values in head order; dK takes the scale after the sum, matching
-// BF16(fl32[alpha (dK^acc - C)]) with dK^acc and C summed over the group.
+// grid owns 8 consecutive elements of one key/value head and adds the G query
+// heads' values in head order, starting from zero; dK takes the scale after
+// the sum, matching BF16(fl32[alpha (dK^acc - C)]) with dK^acc and C summed
+// over the group.  A memory-bound pass: with the group size known at compile
+// time (GC > 0) every load of the thread is issued before the first add.
+template <int GC>
 __global__ __launch_bounds__(256) void group_sum_kernel(const float* __restrict__ dKp,
                                                         const float* __restrict__ dVp,
                                                         uint16_t* __restrict__ dK,
                                                         uint16_t* __restrict__ dV, int BHkv,
-                                                        int G, size_t per_head, float scale) {
-    const size_t quads = per_head / 4;
+                                                        int Grt, size_t per_head, float scale) {
+    const int G = GC > 0 ? GC : Grt;
+    const size_t octs = per_head / 8;
     const size_t t = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= (size_t)BHkv * quads) return;
-    const size_t kvh = t / quads, e = (t - kvh * quads) * 4;
-    f32x4 sk = {0.f, 0.f, 0.f, 0.f}, sv = {0.f, 0.f, 0.f, 0.f};
-    for (int gq = 0; gq < G; ++gq) {
-        const size_t off = (kvh * G + gq) * per_head + e;
-        sk += *reinterpret_cast<const f32x4*>(dKp + off);
-        sv += *reinterpret_cast<const f32x4*>(dVp + off);
-    }
-    float k4[4];
+    if (t >= (size_t)BHkv * octs) return;
+    const size_t kvh = t / octs, e = (t - kvh * octs) * 8;
+    const float* kp = dKp + kvh * G * per_head + e;
+    const float* vp = dVp + kvh * G * per_head + e;
+    f32x4 sk[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+    f32x4 sv[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+    if constexpr (GC > 0) {
+        f32x4 lk[GC][2], lv[GC][2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-#pragma clang fp contract(off)
-        k4[i] = scale * sk[i];
+        for (int gq = 0; gq < GC; ++gq)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                lk[gq][h] = *reinterpret_cast<const f32x4*>(kp + gq * per_head + 4 * h);
+                lv[gq][h] = *reinterpret_cast<const f32x4*>(vp + gq * per_head + 4 * h);
+            }
+#pragma unroll
+        for (int gq = 0; gq < GC; ++gq)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                sk[h] += lk[gq][h];
+                sv[h] += lv[gq][h];
+            }
+    } else {
+        for (int gq = 0; gq < G; ++gq)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                sk[h] += *reinterpret_cast<const f32x4*>(kp + gq * per_head + 4 * h);
+                sv[h] += *reinterpret_cast<const f32x4*>(vp + gq * per_head + 4 * h);
+            }
     }
-    st_bf16x4(dK + kvh * per_head + e, k4[0], k4[1], k4[2], k4[3]);
-    st_bf16x4(dV + kvh * per_head + e, sv[0], sv[1], sv[2], sv[3]);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        float k4[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+#pragma clang fp contract(off)
+            k4[i] = scale * sk[h][i];
+        }
+        st_bf16x4(dK + kvh * per_head + e + 4 * h, k4[0], k4[1], k4[2], k4[3]);
+        st_bf16x4(dV + kvh * per_head + e + 4 * h, sv[h][0], sv[h][1], sv[h][2], sv[h][3]);
+    }
 }
 
 // Preprocessing of the atomic schedule (dense multi-head): Algorithm 1's
@@ -1252,9 +1281,16 @@ hipError_t launch_bwd_group_sum(const float* dKp, const float* dVp, uint16_t* dK
                                 const Shape& s, hipStream_t st) {
     const int BHkv = s.BH / s.G;
     const size_t per_head = (size_t)s.N * s.d;
-    const size_t threads = (size_t)BHkv * (per_head / 4);
+    const size_t threads = (size_t)BHkv * (per_head / 8);
     dim3 grid((unsigned)((threads + 255) / 256)), block(256);
-    launch_kernel(group_sum_kernel, grid, block, st, dKp, dVp, dK, dV, BHkv, s.G, per_head, s.scale);
+#define GPA_GSUM(GC)                                                                       \
+    launch_kernel(group_sum_kernel<GC>, grid, block, st, dKp, dVp, dK, dV, BHkv, s.G, per_head, \
+                  s.scale)
+    if (s.G == 2) GPA_GSUM(2);
+    else if (s.G == 4) GPA_GSUM(4);
+    else if (s.G == 8) GPA_GSUM(8);
+    else GPA_GSUM(0);
+#undef GPA_GSUM
     return hipGetLastError();
 }
 
