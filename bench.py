@@ -478,9 +478,12 @@ def main():
 
     def hbm_entry(name, ms_k, nbytes, what):
         gbs = nbytes / (ms_k * 1e-3) / 1e9
+        kname, kmode = name.rsplit("/", 1)
         hbm[name] = {"ms": round(ms_k, 5), "bytes": int(nbytes), "achieved_GB_s": round(gbs, 1),
                      "peak_GB_s": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4),
-                     "bytes_counted": what}
+                     "bytes_counted": what,
+                     # calibrated FETCH_SIZE + WRITE_SIZE of the committed PMC summary
+                     "traffic": recorded_traffic(kname, kmode)}
 
     ten = B * H * N * d                      # elements of one [B, H, N, d] tensor
     rows = B * H * N
