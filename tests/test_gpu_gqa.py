@@ -112,7 +112,9 @@ def check(gpa, x, causal, scale, tag, blowup_ratio=3.0, rowtile=False):
 
 @pytest.mark.parametrize("B,Hq,Hkv,N,d,causal", [
     (1, 4, 1, 128, 64, True), (1, 4, 2, 200, 64, True), (2, 6, 3, 129, 128, True),
-    (1, 8, 2, 65, 64, False), (1, 2, 1, 1, 64, True)])
+    (1, 8, 2, 65, 64, False), (1, 2, 1, 1, 64, True),
+    # group sizes the group sum handles with a run-time loop (not 2, 4 or 8)
+    (1, 6, 2, 150, 64, True), (1, 16, 1, 70, 128, False)])
 def test_gqa_small(gpa, B, Hq, Hkv, N, d, causal):
     w = S.Workload("gqa", B, Hq, N, d, causal=causal, k_bias_std=8.0, do_std=1.0, Hkv=Hkv)
     x = S.make_inputs(w, 500 + N)
