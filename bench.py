@@ -94,7 +94,8 @@ def recorded_traffic(kernel: str, mode: str, workload: str = "h16_n4096_d64"):
 
 def time_config(gpa, S, wc, seed, iters, dev, to_dev, oracle=None, heads=None):
     """Forward and per-mode backward times of one multi-head workload (mean of
-    `iters` calls after ~100 ms of load), its fwd+bwd TFLOP/s by the standard
+    `iters` calls after ~100 ms of load, and the p10 / median / p90 of `iters`
+    individually timed calls), its fwd+bwd TFLOP/s by the standard
     count, the GProj overhead and every kernel's fraction of the bf16 peak by
     its algorithmic products.  With the oracle, also the relative L2 errors
     (%) of O, dQ, dK, dV in every mode and of the FP32 baseline against the
@@ -118,6 +119,19 @@ def time_config(gpa, S, wc, seed, iters, dev, to_dev, oracle=None, heads=None):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / iters
 
+    def per_call(fn):
+        # p10 / median / p90 of `iters` calls, each between its own events
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(iters)]
+        for a, b in ev:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        t = sorted(a.elapsed_time(b) for a, b in ev)
+        q = lambda f: t[min(len(t) - 1, int(round(f * (len(t) - 1))))]  # noqa: E731
+        return [round(q(0.1), 5), round(q(0.5), 5), round(q(0.9), 5)]
+
     o, lse = gpa.attn_fwd(q, k, v, wc.causal, wc.scale)
     # keep the GPU busy for ~100 ms first, so every mode is timed at the same
     # sustained clock
@@ -129,14 +143,16 @@ def time_config(gpa, S, wc, seed, iters, dev, to_dev, oracle=None, heads=None):
         gpa.attn_bwd(q, k, v, o, lse, u, "gproj", wc.causal, wc.scale, workspace=wsw)
         torch.cuda.synchronize()
     del wsw
+    fwd = lambda: gpa.attn_fwd(q, k, v, wc.causal, wc.scale)  # noqa: E731
     res = {"B": B, "H": H, "N": N, "d": d, "seed": seed, "calls_timed": iters,
-           "fwd_ms": round(timed(lambda: gpa.attn_fwd(q, k, v, wc.causal, wc.scale)), 5),
-           "bwd_ms": {}, "kernel_frac": {}}
+           "fwd_ms": round(timed(fwd), 5), "bwd_ms": {}, "kernel_frac": {},
+           "per_call_ms_p10_p50_p90": {"fwd": per_call(fwd)}}
     pairs = B * H * N * N / 2.0
     for m in gpa.MODES:
         ws = torch.empty(gpa.attn_bwd_workspace_bytes(B, H, N, d, m), dtype=torch.uint8, device=dev)
         fn = lambda: gpa.attn_bwd(q, k, v, o, lse, u, m, wc.causal, wc.scale, workspace=ws)  # noqa: E731
         res["bwd_ms"][m] = round(timed(fn), 5)
+        res["per_call_ms_p10_p50_p90"]["bwd_" + m] = per_call(fn)
         gpa.profile_enable(True)
         for _ in range(iters):
             fn()
@@ -515,7 +531,8 @@ def main():
         orc = None
         if not args.no_accuracy:
             import oracle as orc
-        for idx, iters in ((3, 50), (4, 20), (5, 6)):
+        # at least 50 calls or 200 ms of each: 50, 50, 10 calls
+        for idx, iters in ((3, 50), (4, 50), (5, 10)):
             wc = S.WORKLOADS[idx]
             out["configs"][wc.name] = time_config(
                 gpa, S, wc, 1000 * idx, iters, dev, to_dev,
