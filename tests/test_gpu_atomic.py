@@ -36,7 +36,7 @@ def gpa():
 @pytest.mark.parametrize("mode", ["plain", "gproj_q", "gproj"])
 @pytest.mark.parametrize("B,H,N,d,causal", [
     (1, 2, 200, 64, True), (1, 1, 1, 64, True), (2, 1, 65, 128, True), (1, 2, 130, 64, False),
-    (1, 16, 4096, 64, True)])
+    (1, 1, 100, 128, False), (1, 2, 64, 64, False), (1, 16, 4096, 64, True)])
 def test_atomic_schedule_matches_two_pass(gpa, B, H, N, d, causal, mode):
     w = S.Workload("atomic", B, H, N, d, causal=causal, k_bias_std=4.0,
                    do_std=0.01 if N == 4096 else 1.0)
