@@ -446,6 +446,9 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
     // schedule's B, rho and m.
     constexpr bool ZC = GPROJ && !FUSED_DQ;
     constexpr bool AB = GPROJ && FUSED_DQ;
+    // d = 128 runs one wave per SIMD: order each step for the wave's own
+    // overlap of vector and matrix work (see the step).
+    constexpr bool PIPE = D == 128 && !FUSED_DQ;
     constexpr int NT = ZC ? 3 : 2;  // staged tensors: Q, dO (and Z = BF16(lambda Q))
     // Accumulators per output element: dV, and dK^acc - C in one (the GProj
     // pass adds t^T Q and r^T (-z) into the same FP32 accumulator).
@@ -588,67 +591,129 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DKDV_OCC64 : 1) void bwd_dk
             l2[mq] = *reinterpret_cast<const f32x4*>(st + mq * 16 + 4 * g);
             dd[mq] = *reinterpret_cast<const f32x4*>(st + 32 + mq * 16 + 4 * g);
         }
-        // The transposed A operands of the first two column blocks of the
-        // dV/dK/C products are read now, so their LDS latency hides behind the
-        // S/dP products and the exponentials.
-        bf16x8 opd[2][NT];
-        auto read_ops = [&](bf16x8 (&o)[NT], int mb) {
-            o[0] = ld_tr_operand<D>(Uc, 32 * qh, mb * 16, c16, g);
-            o[1] = ld_tr_operand<D>(Qc, 32 * qh, mb * 16, c16, g);
-            if (ZC) o[NT - 1] = ld_tr_operand<D>(Zc, 32 * qh, mb * 16, c16, g);
-        };
-        read_ops(opd[0], 0);
-        read_ops(opd[1], 1);
-        __builtin_amdgcn_sched_barrier(0);
-
-        // S = Q K^T and dP = dO V^T for this wave's 32 queries x 32 keys, one
-        // 16 x 16 block at a time: s holds queries 4g+i of query block mq for
-        // key block kb, and P, r, t of that block go straight into half mq of
-        // the key block's B operands tf[kb], rf[kb].
         bf16x8 tf[2], rf[2];
-        // Raise this wave's issue priority while it feeds the matrix core, so
-        // that the other wave on the SIMD fills the vector ALU meanwhile.
-        __builtin_amdgcn_s_setprio(1);
-        // LLVM's interleaving strategy 1 for matrix-core and LDS instructions
-        // (measured 1.5-2 % faster here; neutral in the query pass).
-        __builtin_amdgcn_iglp_opt(1);
+        if constexpr (PIPE) {
+            // One wave per SIMD (d = 128): no second wave fills the vector
+            // ALU while this one multiplies, so the step is ordered by key
+            // block instead, for the wave's own co-issue: S/dP of key block 0,
+            // then S/dP of block 1 beside the probabilities of block 0, then
+            // the dV/dK/C products of block 0 beside the probabilities of
+            // block 1, then the products of block 1.  Every accumulator still
+            // receives its products in the same order.
+            bf16x8 qa[2][KC], ua[2][KC];
 #pragma unroll
-        for (int mq = 0; mq < 2; ++mq) {
-            const int row = 32 * qh + mq * 16 + c16;
-            bf16x8 qa[KC], ua[KC];
-#pragma unroll
-            for (int kc = 0; kc < KC; ++kc) {
-                qa[kc] = ld_b128(Qc + tile_off<D>(row, kc * 32 + 8 * g));
-                ua[kc] = ld_b128(Uc + tile_off<D>(row, kc * 32 + 8 * g));
-            }
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                f32x4 sv = {0.f, 0.f, 0.f, 0.f}, dpv = {0.f, 0.f, 0.f, 0.f};
+            for (int mq = 0; mq < 2; ++mq)
 #pragma unroll
                 for (int kc = 0; kc < KC; ++kc) {
-                    sv = mfma_16x16x32(qa[kc], kf[kb][kc], sv);
-                    dpv = mfma_16x16x32(ua[kc], vf[kb][kc], dpv);
+                    const int row = 32 * qh + mq * 16 + c16;
+                    qa[mq][kc] = ld_b128(Qc + tile_off<D>(row, kc * 32 + 8 * g));
+                    ua[mq][kc] = ld_b128(Uc + tile_off<D>(row, kc * 32 + 8 * g));
                 }
-                dkdv_probs<MASK>(sv, dpv, l2[mq], dd[mq], c, q0 + 32 * qh + mq * 16, g,
-                                 k0w + kb * 16 + c16, moff, mq, tf[kb], rf[kb]);
-                fill_piece(nxt2, qt + 2, AT_START + mq * 2 + kb);
-            }
-        }
-        // dV^T[dv][key] += dO^T r ; dK^T += Q^T t ; C^T += Z^T r.  The A operands
-        // of column block mb + 2 are read from LDS while block mb multiplies.
-        __builtin_amdgcn_s_setprio(0);
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-            const bf16x8* o = opd[mb & 1];
-            const bf16x8 ua = o[0], qa = o[1], za = o[NT - 1];
+            // LLVM's small-GEMM interleaving strategy for this order (measured
+            // 3-4 % faster than strategy 1 here, which pairs each product with
+            // an LDS read issued just before it).
+            __builtin_amdgcn_iglp_opt(0);
+            f32x4 sv[2][2], dpv[2][2];  // [kb][mq]
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
-                accV[kb][mb] = mfma_16x16x32(ua, rf[kb], accV[kb][mb]);
-                accK[kb][mb] = mfma_16x16x32(qa, tf[kb], accK[kb][mb]);
-                if (ZC) accK[kb][mb] = mfma_16x16x32(za, rf[kb], accK[kb][mb]);
+#pragma unroll
+                for (int mq = 0; mq < 2; ++mq) {
+                    sv[kb][mq] = f32x4{0.f, 0.f, 0.f, 0.f};
+                    dpv[kb][mq] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int kc = 0; kc < KC; ++kc) {
+                        sv[kb][mq] = mfma_16x16x32(qa[mq][kc], kf[kb][kc], sv[kb][mq]);
+                        dpv[kb][mq] = mfma_16x16x32(ua[mq][kc], vf[kb][kc], dpv[kb][mq]);
+                    }
+                    fill_piece(nxt2, qt + 2, AT_START + kb * 2 + mq);
+                }
             }
-            if (mb + 2 < MB) read_ops(opd[mb & 1], mb + 2);
-            fill_piece(nxt2, qt + 2, AT_START + 4 + mb);
+            // The transposed A operands of every column block, held for both
+            // key blocks.
+            bf16x8 opd[MB][NT];
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+                opd[mb][0] = ld_tr_operand<D>(Uc, 32 * qh, mb * 16, c16, g);
+                opd[mb][1] = ld_tr_operand<D>(Qc, 32 * qh, mb * 16, c16, g);
+                if (ZC) opd[mb][NT - 1] = ld_tr_operand<D>(Zc, 32 * qh, mb * 16, c16, g);
+            }
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+                for (int mq = 0; mq < 2; ++mq)
+                    dkdv_probs<MASK>(sv[kb][mq], dpv[kb][mq], l2[mq], dd[mq], c,
+                                     q0 + 32 * qh + mq * 16, g, k0w + kb * 16 + c16, moff, mq,
+                                     tf[kb], rf[kb]);
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) {
+                    accV[kb][mb] = mfma_16x16x32(opd[mb][0], rf[kb], accV[kb][mb]);
+                    accK[kb][mb] = mfma_16x16x32(opd[mb][1], tf[kb], accK[kb][mb]);
+                    if (ZC) accK[kb][mb] = mfma_16x16x32(opd[mb][NT - 1], rf[kb], accK[kb][mb]);
+                    if (kb == 1) fill_piece(nxt2, qt + 2, AT_START + 4 + mb);
+                }
+            }
+        } else {
+            // The transposed A operands of the first two column blocks of the
+            // dV/dK/C products are read now, so their LDS latency hides behind the
+            // S/dP products and the exponentials.
+            bf16x8 opd[2][NT];
+            auto read_ops = [&](bf16x8 (&o)[NT], int mb) {
+                o[0] = ld_tr_operand<D>(Uc, 32 * qh, mb * 16, c16, g);
+                o[1] = ld_tr_operand<D>(Qc, 32 * qh, mb * 16, c16, g);
+                if (ZC) o[NT - 1] = ld_tr_operand<D>(Zc, 32 * qh, mb * 16, c16, g);
+            };
+            read_ops(opd[0], 0);
+            read_ops(opd[1], 1);
+            __builtin_amdgcn_sched_barrier(0);
+
+            // S = Q K^T and dP = dO V^T for this wave's 32 queries x 32 keys, one
+            // 16 x 16 block at a time: s holds queries 4g+i of query block mq for
+            // key block kb, and P, r, t of that block go straight into half mq of
+            // the key block's B operands tf[kb], rf[kb].
+            // Raise this wave's issue priority while it feeds the matrix core, so
+            // that the other wave on the SIMD fills the vector ALU meanwhile.
+            __builtin_amdgcn_s_setprio(1);
+            // LLVM's interleaving strategy 1 for matrix-core and LDS instructions
+            // (measured 1.5-2 % faster here; neutral in the query pass).
+            __builtin_amdgcn_iglp_opt(1);
+    #pragma unroll
+            for (int mq = 0; mq < 2; ++mq) {
+                const int row = 32 * qh + mq * 16 + c16;
+                bf16x8 qa[KC], ua[KC];
+    #pragma unroll
+                for (int kc = 0; kc < KC; ++kc) {
+                    qa[kc] = ld_b128(Qc + tile_off<D>(row, kc * 32 + 8 * g));
+                    ua[kc] = ld_b128(Uc + tile_off<D>(row, kc * 32 + 8 * g));
+                }
+    #pragma unroll
+                for (int kb = 0; kb < 2; ++kb) {
+                    f32x4 sv = {0.f, 0.f, 0.f, 0.f}, dpv = {0.f, 0.f, 0.f, 0.f};
+    #pragma unroll
+                    for (int kc = 0; kc < KC; ++kc) {
+                        sv = mfma_16x16x32(qa[kc], kf[kb][kc], sv);
+                        dpv = mfma_16x16x32(ua[kc], vf[kb][kc], dpv);
+                    }
+                    dkdv_probs<MASK>(sv, dpv, l2[mq], dd[mq], c, q0 + 32 * qh + mq * 16, g,
+                                     k0w + kb * 16 + c16, moff, mq, tf[kb], rf[kb]);
+                    fill_piece(nxt2, qt + 2, AT_START + mq * 2 + kb);
+                }
+            }
+            // dV^T[dv][key] += dO^T r ; dK^T += Q^T t ; C^T += Z^T r.  The A operands
+            // of column block mb + 2 are read from LDS while block mb multiplies.
+            __builtin_amdgcn_s_setprio(0);
+    #pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+                const bf16x8* o = opd[mb & 1];
+                const bf16x8 ua = o[0], qa = o[1], za = o[NT - 1];
+    #pragma unroll
+                for (int kb = 0; kb < 2; ++kb) {
+                    accV[kb][mb] = mfma_16x16x32(ua, rf[kb], accV[kb][mb]);
+                    accK[kb][mb] = mfma_16x16x32(qa, tf[kb], accK[kb][mb]);
+                    if (ZC) accK[kb][mb] = mfma_16x16x32(za, rf[kb], accK[kb][mb]);
+                }
+                if (mb + 2 < MB) read_ops(opd[mb & 1], mb + 2);
+                fill_piece(nxt2, qt + 2, AT_START + 4 + mb);
+            }
         }
         if constexpr (FUSED_DQ) {
             // t of this wave's 32 keys x 32 queries into Xt[key][query] (r
