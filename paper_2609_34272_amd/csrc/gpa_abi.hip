@@ -105,8 +105,7 @@ hipEvent_t take_event() {
 // With timing on, the launcher's kernel records the pair of events at its own
 // start and end (launch_kernel), so each record is one kernel's duration.
 template <class F>
-hipError_t timed(int id, hipStream_t st, F&& launch) {
-    (void)st;
+hipError_t timed(int id, F&& launch) {
     if (!g_prof) return launch();
     hipEvent_t a = take_event(), b = take_event();
     gpa::launch_events() = {a, b};
@@ -214,7 +213,7 @@ gpa_status run_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, cons
     float* dkp = sh.G > 1 ? (float*)(ws + L.dkp) : nullptr;
     float* dvp = sh.G > 1 ? (float*)(ws + L.dvp) : nullptr;
 
-    gpa_status s = launched(timed(gpa::kKBwdDq, st,
+    gpa_status s = launched(timed(gpa::kKBwdDq,
                                   [&] {
                                       return gpa::launch_bwd_dq(Q, K, V, O, dO, LSE, Drow, tstats,
                                                                 dQ, rho, msum, lam, zbuf, mode, sh,
@@ -222,7 +221,7 @@ gpa_status run_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, cons
                                   }),
                             "bwd_dq");
     if (s != GPA_OK) return s;
-    s = launched(timed(gpa::kKBwdDkdv, st,
+    s = launched(timed(gpa::kKBwdDkdv,
                        [&] {
                            return gpa::launch_bwd_dkdv(Q, K, V, dO, tstats, zbuf, dK, dV, dkp, dvp,
                                                        mode, sh, st);
@@ -234,7 +233,7 @@ gpa_status run_bwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V, cons
     gpa::Shape gs = sh;
     gs.BH = sh.cu ? sh.Hq : sh.BH;
     gs.N = (int)(krows / (size_t)gs.BH);
-    return launched(timed(gpa::kKGroupSum, st,
+    return launched(timed(gpa::kKGroupSum,
                           [&] { return gpa::launch_bwd_group_sum(dkp, dvp, dK, dV, gs, st); }),
                     "group_sum");
 }
@@ -389,7 +388,7 @@ gpa_status gpa_attn_fwd_gqa(const uint16_t* Q, const uint16_t* K, const uint16_t
     if (s != GPA_OK) return s;
     const gpa::Shape sh{(int)(B * Hq), (int)N, (int)d, causal ? 1 : 0, scale, (int)(Hq / Hkv)};
     hipStream_t st = (hipStream_t)stream;
-    return launched(timed(gpa::kKFwd, st, [&] { return gpa::launch_fwd(Q, K, V, O, LSE, sh, st); }),
+    return launched(timed(gpa::kKFwd, [&] { return gpa::launch_fwd(Q, K, V, O, LSE, sh, st); }),
                     "fwd_sbs");
 }
 
@@ -410,7 +409,7 @@ gpa_status gpa_attn_fwd_fma(const uint16_t* Q, const uint16_t* K, const uint16_t
     const gpa::Shape sh{(int)(B * H), (int)N, (int)d, causal ? 1 : 0, scale, 1};
     hipStream_t st = (hipStream_t)stream;
     return launched(
-        timed(gpa::kKFwd, st, [&] { return gpa::launch_fwd(Q, K, V, O, LSE, sh, st, true); }),
+        timed(gpa::kKFwd, [&] { return gpa::launch_fwd(Q, K, V, O, LSE, sh, st, true); }),
         "fwd_fma");
 }
 
@@ -545,11 +544,11 @@ gpa_status gpa_attn_bwd_atomic(const uint16_t* Q, const uint16_t* K, const uint1
     }
     if (mode == 2) acc.dKacc = (float*)(w + l.dkacc);
     uint16_t* Zneg = mode == 2 ? (uint16_t*)(w + l.z) : nullptr;
-    s = launched(timed(gpa::kKBwdPre, st,
+    s = launched(timed(gpa::kKBwdPre,
                        [&] { return gpa::launch_bwd_pre(O, dO, LSE, TS, acc, sh, st); }),
                  "bwd_pre");
     if (s != GPA_OK) return s;
-    s = launched(timed(gpa::kKBwdFused, st,
+    s = launched(timed(gpa::kKBwdFused,
                        [&] {
                            return gpa::launch_bwd_fused(Q, K, V, dO, TS, dK, dV, acc, mode, sh,
                                                         st);
@@ -557,17 +556,17 @@ gpa_status gpa_attn_bwd_atomic(const uint16_t* Q, const uint16_t* K, const uint1
                  "bwd_fused");
     if (s != GPA_OK) return s;
     if (mode == 0)
-        return launched(timed(gpa::kKBwdFinal, st,
+        return launched(timed(gpa::kKBwdFinal,
                               [&] { return gpa::launch_bwd_dq_finalize(acc.A, dQ, sh, st); }),
                         "bwd_dq_finalize");
-    s = launched(timed(gpa::kKBwdFinal, st,
+    s = launched(timed(gpa::kKBwdFinal,
                        [&] {
                            return gpa::launch_bwd_gproj_finalize(acc, Q, dQ, Zneg, nullptr, sh,
                                                                  st);
                        }),
                  "bwd_gproj_finalize");
     if (s != GPA_OK || mode == 1) return s;
-    return launched(timed(gpa::kKBwdCorr, st,
+    return launched(timed(gpa::kKBwdCorr,
                           [&] {
                               return gpa::launch_bwd_dk_corr(Q, K, TS, Zneg, acc.dKacc, dK, sh, st);
                           }),
@@ -592,7 +591,7 @@ gpa_status gpa_attn_fwd_varlen(const uint16_t* Q, const uint16_t* K, const uint1
     if ((s = check_cu_overlap(v, outs)) != GPA_OK) return s;
     const gpa::Shape sh = varlen_shape(v, causal, scale);
     hipStream_t st = (hipStream_t)stream;
-    return launched(timed(gpa::kKFwd, st, [&] { return gpa::launch_fwd(Q, K, V, O, LSE, sh, st); }),
+    return launched(timed(gpa::kKFwd, [&] { return gpa::launch_fwd(Q, K, V, O, LSE, sh, st); }),
                     "fwd_sbs");
 }
 
@@ -676,17 +675,17 @@ gpa_status gpa_fp32_attn(const uint16_t* Q, const uint16_t* K, const uint16_t* V
     float* Mrow = (float*)(ws + L.mrow);
     float* Linv = (float*)(ws + L.linv);
     float* TS = (float*)(ws + L.ts);
-    s = launched(timed(gpa::kKF32Fwd, st,
+    s = launched(timed(gpa::kKF32Fwd,
                        [&] { return gpa::launch_f32_fwd(Q, K, V, O32, O, LSE, Mrow, Linv, sh, st); }),
                  "fp32_fwd");
     if (s != GPA_OK) return s;
-    s = launched(timed(gpa::kKF32Dq, st,
+    s = launched(timed(gpa::kKF32Dq,
                        [&] {
                            return gpa::launch_f32_dq(Q, K, V, dO, O32, Mrow, Linv, TS, dQ, sh, st);
                        }),
                  "fp32_dq");
     if (s != GPA_OK) return s;
-    return launched(timed(gpa::kKF32Dkdv, st,
+    return launched(timed(gpa::kKF32Dkdv,
                           [&] { return gpa::launch_f32_dkdv(Q, K, V, dO, TS, dK, dV, sh, st); }),
                     "fp32_dkdv");
 }
