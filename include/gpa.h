@@ -325,7 +325,8 @@ gpa_status gpa_fp32_attn(const uint16_t* Q, const uint16_t* K, const uint16_t* V
  * stream (hipExtLaunchKernel's start and stop events).  gpa_profile_read
  * synchronises those events, writes per-kernel totals (milliseconds) and launch
  * counts for kernel ids 0..n-1 (see gpa_kernel_name), clears them, and
- * returns the number of ids.  Not thread-safe; meant for benchmarks.
+ * returns the number of ids.  Not thread-safe and not for calls under stream
+ * capture (keep it off while capturing a graph); meant for benchmarks.
  */
 void gpa_profile_enable(int on);
 int gpa_profile_read(double* total_ms, int64_t* launches, int n);
