@@ -129,7 +129,11 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
         // their whole latency.
         __builtin_amdgcn_sched_barrier(0);
         // S^T[key][query] for this wave's 32 keys x 32 queries; s[nb][kb]
-        // holds keys 4g+i of key block kb for query block nb.
+        // holds keys 4g+i of key block kb for query block nb.  The wave raises
+        // its issue priority while it feeds the matrix core, so that the other
+        // wave on the SIMD runs its exponentials meanwhile (h16_n4096_d128
+        // forward 6 % faster; neutral on the batched d = 128 workload).
+        __builtin_amdgcn_s_setprio(1);
         f32x4 s[2][2];
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
@@ -155,6 +159,7 @@ __global__ __launch_bounds__(kThreads, GPA_FWD_OCC) void fwd_sbs_kernel(
                         s[nb][kb][i] = ok ? s[nb][kb][i] : -INFINITY;
                     }
         }
+        __builtin_amdgcn_s_setprio(0);
         bf16x8 pf[2];
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb) {
