@@ -28,7 +28,10 @@
 // Work split inside a workgroup (4 waves).  Each wave owns 32 of the
 // workgroup's 64 rows (two 16-row MFMA blocks that share every LDS operand
 // fragment) and half of each streamed tile; the two waves that own the same
-// rows add their partial accumulators through LDS at the end.
+// rows add their partial accumulators through LDS at the end.  The d = 128
+// query pass, whose 32-row waves fill the register file (one wave per SIMD),
+// runs 8 waves of one 16-row block each instead: two waves per SIMD, each K
+// and V fragment feeding one MFMA instead of two.
 //
 // MFMA layouts (v_mfma_f32_16x16x32_bf16, wave64): an A operand holds one row
 // per lane (row = lane & 15) and 8 values along k; a B operand holds one column
@@ -47,25 +50,25 @@
 namespace gpa {
 namespace {
 
-// Pairwise reduction of per-lane FP32 partials between waves w and w + 2:
-// waves 2, 3 park their values in LDS (lane-contiguous, conflict-free), waves
-// 0, 1 add them.  `scratch` holds CAP floats; the values go through it in
-// rounds of CAP / 128 per lane.  The caller has synchronised the workgroup so
+// Pairwise reduction of per-lane FP32 partials between waves w and w + QG:
+// waves QG .. 2 QG - 1 park their values in LDS (lane-contiguous,
+// conflict-free), waves 0 .. QG - 1 add them.  `scratch` holds CAP floats;
+// the values go through it in rounds of CAP / (64 QG) per lane.  The caller has synchronised the workgroup so
 // the buffer is free; on return it is free again only after a barrier.
-template <int NV, int CAP>
+template <int NV, int CAP, int QG = 2>
 __device__ __forceinline__ void pair_reduce(float (&v)[NV], float* scratch, int wave, int lane) {
-    constexpr int PER = CAP / 128;
+    constexpr int PER = CAP / (64 * QG);
     static_assert(PER >= 1, "scratch too small");
 #pragma unroll
     for (int j0 = 0; j0 < NV; j0 += PER) {
         if (j0) __syncthreads();
-        if (wave >= 2) {
-            float* p = scratch + (wave - 2) * 64 * PER + lane;
+        if (wave >= QG) {
+            float* p = scratch + (wave - QG) * 64 * PER + lane;
 #pragma unroll
             for (int j = j0; j < (j0 + PER < NV ? j0 + PER : NV); ++j) p[(j - j0) * 64] = v[j];
         }
         __syncthreads();
-        if (wave < 2) {
+        if (wave < QG) {
             const float* p = scratch + wave * 64 * PER + lane;
 #pragma unroll
             for (int j = j0; j < (j0 + PER < NV ? j0 + PER : NV); ++j) v[j] += p[(j - j0) * 64];
@@ -101,8 +104,8 @@ __device__ __forceinline__ void dq_probs(const f32x4 (&s)[2], const f32x4 (&dp)[
         }
 }
 
-template <int D, bool GPROJ, bool WRITE_Z>
-__global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_kernel(
+template <int D, bool GPROJ, bool WRITE_Z, int NB = 2>
+__global__ __launch_bounds__(kThreads * 2 / NB, D == 64 ? GPA_DQ_OCC64 : 2 / NB) void bwd_dq_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, const uint16_t* __restrict__ O,
     const uint16_t* __restrict__ dO, const float* __restrict__ LSE, float* __restrict__ D_out,
@@ -114,6 +117,10 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     constexpr int MB = D / 16;  // 16-column blocks of d
     constexpr int KC = D / 32;  // 32-wide k chunks of d
     constexpr int PER_NB = 2 * MB * 4 + 2;  // partial A, B (interleaved) and rho, m
+    // NB 16-row query blocks per wave: QG groups of waves own the 64 rows,
+    // two waves (the two key halves of each tile) per group.
+    constexpr int QG = 4 / NB;
+    constexpr int NTHR = 64 * 2 * QG;
     // A three-slot ring of [K tile, V tile] (row-major, swizzled): while tile
     // i is computed on, tiles i+1 and i+2 are in flight.  Slot 0 is reused at
     // the end for the pairwise reduction.
@@ -136,9 +143,9 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, c16 = lane & 15;
-    const int qh = wave & 1;   // which 32 of the workgroup's 64 queries
-    const int kh = wave >> 1;  // which 32 of each 64-key tile
-    const int q0w = tile * kTile + 32 * qh;
+    const int qh = wave % QG;  // which 16 NB of the workgroup's 64 queries
+    const int kh = wave / QG;  // which 32 of each 64-key tile
+    const int q0w = tile * kTile + 16 * NB * qh;
 
     // Q^T and dO^T as B operands: column = this lane's query of block nb, k = d.
     // Rows beyond N load as zero.
@@ -146,10 +153,10 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     const rsrc_t rq = make_rsrc(Q + hoff, tbytes);
     const rsrc_t ru = make_rsrc(dO + hoff, tbytes);
     const rsrc_t ro = make_rsrc(O + hoff, tbytes);
-    bf16x8 qf[2][KC], uf[2][KC];
-    float lse2[2], Di[2];
+    bf16x8 qf[NB][KC], uf[NB][KC];
+    float lse2[NB], Di[NB];
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
+    for (int nb = 0; nb < NB; ++nb) {
         const int qrow = q0w + nb * 16 + c16;
         float dpart = 0.f;
 #pragma unroll
@@ -174,9 +181,9 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     const float c = scale * kLog2e;
     const bf16x8 ones = ones_row0(c16);
 
-    f32x4 accA[2][MB], accB[2][GPROJ ? MB : 1], accR[2], accM[2];
+    f32x4 accA[NB][MB], accB[NB][GPROJ ? MB : 1], accR[NB], accM[NB];
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
+    for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) accA[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -192,14 +199,15 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
     const KeyRange kr = key_range(tile, Nk, off, causal);
     const int nkv = kr.nkv, nplain = kr.nplain;
 
-    TileDma<D> dma;
+    TileDma<D, NTHR> dma;
     dma.init(lane, wave);
     // Piece j of the fill of `slot` with key tile kt (K calls, then V calls);
     // past the last tile it is a zero fill, so every step issues FILL_VM loads.
-    constexpr int FILL_VM = 2 * TileDma<D>::CALLS;
+    constexpr int CALLS = TileDma<D, NTHR>::CALLS;
+    constexpr int FILL_VM = 2 * CALLS;
     auto fill_piece = [&](uint16_t* slot, int kt, int j) {
         if (j < FILL_VM) {
-            const int t = j / TileDma<D>::CALLS, k = j % TileDma<D>::CALLS;
+            const int t = j / CALLS, k = j % CALLS;
             dma.load_call(t ? V + kvoff : K + kvoff, slot + t * TILE_E, kt * kTile, Nk, kt < nkv, k);
         }
     };
@@ -238,11 +246,11 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
         // faster there in every mode; neutral at d = 64, which keeps the
         // default schedule).
         if constexpr (D == 128) __builtin_amdgcn_iglp_opt(1);
-        f32x4 s[2][2], dp[2][2];
+        f32x4 s[NB][2], dp[NB][2];
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
+            for (int nb = 0; nb < NB; ++nb) {
                 s[nb][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
                 dp[nb][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
             }
@@ -252,16 +260,16 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
                 const bf16x8 ka = ld_b128(Kc + tile_off<D>(row, kc * 32 + 8 * g));
                 const bf16x8 va = ld_b128(Vc + tile_off<D>(row, kc * 32 + 8 * g));
 #pragma unroll
-                for (int nb = 0; nb < 2; ++nb) {
+                for (int nb = 0; nb < NB; ++nb) {
                     s[nb][kb] = mfma_16x16x32(ka, qf[nb][kc], s[nb][kb]);
                     dp[nb][kb] = mfma_16x16x32(va, uf[nb][kc], dp[nb][kb]);
                 }
             }
             fill_piece(nxt2, kt + 2, 1 + kb);
         }
-        bf16x8 tf[2], rf[2];
+        bf16x8 tf[NB], rf[NB];
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < NB; ++nb)
             dq_probs<MASK>(s[nb], dp[nb], c, lse2[nb], Di[nb], k0 + 32 * kh, g,
                            q0w + nb * 16 + c16, Nk, causal, off, tf[nb], rf[nb]);
         // A^T[d][query] += K^T[d][key] t^T[key][query] (and B^T with r); the
@@ -272,7 +280,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
             const bf16x8 ka =
                 mb < PF ? ktr[mb < PF ? mb : 0] : ld_tr_operand<D>(Kc, 32 * kh, mb * 16, c16, g);
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
+            for (int nb = 0; nb < NB; ++nb) {
                 accA[nb][mb] = mfma_16x16x32(ka, tf[nb], accA[nb][mb]);
                 if (GPROJ) accB[nb][mb] = mfma_16x16x32(ka, rf[nb], accB[nb][mb]);
             }
@@ -280,7 +288,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
         }
         if (GPROJ) {
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
+            for (int nb = 0; nb < NB; ++nb) {
                 accR[nb] = mfma_16x16x32(ones, tf[nb], accR[nb]);
                 accM[nb] = mfma_16x16x32(ones, rf[nb], accM[nb]);
             }
@@ -314,9 +322,9 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
 
     // Add the partials of the two waves that own the same queries (one query
     // block at a time, to bound the LDS the exchange needs).
-    float red[2][PER_NB];
+    float red[NB][PER_NB];
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
+    for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -327,12 +335,12 @@ __global__ __launch_bounds__(kThreads, D == 64 ? GPA_DQ_OCC64 : 1) void bwd_dq_k
         red[nb][2 * MB * 4] = accR[nb][0];
         red[nb][2 * MB * 4 + 1] = accM[nb][0];
         if (nb) __syncthreads();  // the previous exchange has been read
-        pair_reduce<PER_NB, sizeof(S0) / 4>(red[nb], reinterpret_cast<float*>(S0), wave, lane);
+        pair_reduce<PER_NB, sizeof(S0) / 4, QG>(red[nb], reinterpret_cast<float*>(S0), wave, lane);
     }
-    if (wave >= 2) return;
+    if (wave >= QG) return;
 
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
+    for (int nb = 0; nb < NB; ++nb) {
         const int qrow = q0w + nb * 16 + c16;
         // rho and m of this lane's query sit in accumulator row 0 (lanes g == 0).
         float lam = 0.f, rho = 0.f, msum = 0.f;
@@ -1308,18 +1316,21 @@ hipError_t launch_bwd_dq(const uint16_t* Q, const uint16_t* K, const uint16_t* V
     const int T = (s.N + kTile - 1) / kTile;
     const int Nk = s.Nk > 0 ? s.Nk : s.N;
     dim3 grid((unsigned)(s.BH * T)), block(kThreads);
-#define GPA_DQ(DD, GP, WZ)                                                                   \
-    launch_kernel(bwd_dq_kernel<DD, GP, WZ>, grid, block, st, Q, K, V, O, dO, LSE, Drow, TS, \
-                  dQ, rho, msum, lambda, Z, s.BH, s.N, s.causal, s.scale, s.G, s.cu, s.Hq,   \
+#define GPA_DQ(DD, GP, WZ, NB)                                                                \
+    launch_kernel(bwd_dq_kernel<DD, GP, WZ, NB>, grid, block, st, Q, K, V, O, dO, LSE, Drow, TS, \
+                  dQ, rho, msum, lambda, Z, s.BH, s.N, s.causal, s.scale, s.G, s.cu, s.Hq,    \
                   s.total, s.cu_k, s.total_k, Nk)
     if (s.d == 64) {
-        if (mode == 2) GPA_DQ(64, true, true);
-        else if (mode == 1) GPA_DQ(64, true, false);
-        else GPA_DQ(64, false, false);
+        if (mode == 2) GPA_DQ(64, true, true, 2);
+        else if (mode == 1) GPA_DQ(64, true, false, 2);
+        else GPA_DQ(64, false, false, 2);
     } else {
-        if (mode == 2) GPA_DQ(128, true, true);
-        else if (mode == 1) GPA_DQ(128, true, false);
-        else GPA_DQ(128, false, false);
+        // eight waves of one 16-row query block each (measured 5-8 % faster in
+        // the GProj modes, bitwise the same outputs)
+        block = dim3(2 * kThreads);
+        if (mode == 2) GPA_DQ(128, true, true, 1);
+        else if (mode == 1) GPA_DQ(128, true, false, 1);
+        else GPA_DQ(128, false, false, 1);
     }
 #undef GPA_DQ
     return hipGetLastError();
