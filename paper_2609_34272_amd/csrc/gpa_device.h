@@ -14,9 +14,10 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 // FP32 log2(e), rounded to FP32.
 constexpr float kLog2e = 1.44269504088896340736f;
 
-// Tile geometry shared by the MFMA kernels.  A wave owns 16 rows of its
+// Tile geometry shared by the MFMA kernels.  A wave owns 16 or 32 rows of its
 // operand (queries in the forward and the query-major backward, keys in the
-// key-major backward); a workgroup has 4 waves.
+// key-major backward); a workgroup has 4 waves (the d = 128 query-major pass,
+// 8).
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kTile = 64;  // rows per workgroup tile and per streamed tile
