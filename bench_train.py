@@ -13,9 +13,12 @@ layers.  The model is this script's own stand-in with about 0.43 B parameters
 encoding), randomly initialised and fed random tokens: only the step time
 means anything.  Everything except attention runs on PyTorch's own kernels.
 
-Prints one JSON line with the mean step time per mode (plain, gproj_q,
-gproj; modes interleaved over rounds), the GProj overhead over plain and the
-attention share measured with the library's kernel timers.
+Prints one JSON line with the step time per mode (plain, gproj_q, gproj;
+modes interleaved over rounds: fastest and median round, and the paired
+per-round difference from plain with its standard error), the GProj
+overhead over plain, and the attention kernel time per step in each mode
+measured with the library's kernel timers (the overhead that attention adds
+to a step, without the step-to-step noise of the rest of the model).
 """
 from __future__ import annotations
 
@@ -148,15 +151,29 @@ def main():
     # interleaved rounds is the stable figure (the median is reported too).
     ms = {m: min(t) for m, t in times.items()}
     med = {m: sorted(t)[len(t) // 2] for m, t in times.items()}
-    # attention kernel time inside one gproj step
-    set_mode("gproj")
-    gpa.profile_enable(True)
-    step()
-    torch.cuda.synchronize()
-    prof = gpa.profile_read()
-    gpa.profile_enable(False)
-    attn_ms = sum(t for t, c in prof.values())
-    calls = {k: c for k, (t, c) in prof.items() if c}
+    # Paired per-round differences (the modes of one round run back to back,
+    # so slow drifts of the clock cancel): mean and standard error.
+    def paired(m):
+        d = [a - b for a, b in zip(times[m], times["plain"])]
+        mean = sum(d) / len(d)
+        var = sum((x - mean) ** 2 for x in d) / max(1, len(d) - 1)
+        return round(mean, 3), round((var / len(d)) ** 0.5, 3)
+    # Attention kernel time inside the steps of each mode (the library's
+    # per-kernel event timers, a few steps per mode): a far less noisy measure
+    # of what the mode adds to a step than the step times themselves.
+    attn = {}
+    calls = {}
+    for m in modes:
+        set_mode(m)
+        gpa.profile_enable(True)
+        for _ in range(3):
+            step()
+        torch.cuda.synchronize()
+        prof = gpa.profile_read()
+        gpa.profile_enable(False)
+        attn[m] = sum(t for t, c in prof.values()) / 3
+        if m == "gproj":
+            calls = {k: c // 3 for k, (t, c) in prof.items() if c}
     out = {
         "metric": "training step ms, synthetic 0.43B decoder (B=1, N=4096, 16/4 heads, d=64)",
         "unit": "ms", "higher_is_better": False, "data": "synthetic",
@@ -166,8 +183,13 @@ def main():
         "ms_per_step_rounds": {m: [round(x, 3) for x in v] for m, v in times.items()},
         "gproj_step_overhead_vs_plain_pct": round(100 * (ms["gproj"] / ms["plain"] - 1), 2),
         "gproj_q_step_overhead_vs_plain_pct": round(100 * (ms["gproj_q"] / ms["plain"] - 1), 2),
-        "attention_ms_per_gproj_step": round(attn_ms, 3),
-        "attention_launches_per_step": calls,
+        "paired_step_difference_vs_plain_ms_mean_stderr": {m: paired(m) for m in ("gproj_q", "gproj")},
+        "attention_ms_per_step": {m: round(v, 3) for m, v in attn.items()},
+        "gproj_step_overhead_from_attention_time_pct": round(
+            100 * (attn["gproj"] - attn["plain"]) / ms["plain"], 2),
+        "gproj_q_step_overhead_from_attention_time_pct": round(
+            100 * (attn["gproj_q"] - attn["plain"]) / ms["plain"], 2),
+        "attention_launches_per_gproj_step": calls,
         "peak_allocated_gib": round(torch.cuda.max_memory_allocated() / 2 ** 30, 3),
     }
     print(json.dumps(out), flush=True)
