@@ -92,6 +92,12 @@ gpa_status gpa_attn_fwd(const uint16_t* Q, const uint16_t* K, const uint16_t* V,
  * entry do not matter.  It holds the FP32 row statistics D, rho, m, lambda
  * ([B,H,N] each), a per-64-row-tile copy of log2-scaled LSE and D for the
  * key-major pass, and in gproj mode the BF16 [B,H,N,d] tensor -z = BF16(-lambda q).
+ * (The paper's schedule adds a query-shaped FP32 workspace and two FP32 row
+ * statistics to the native backward: appendix "Implemented Arithmetic and
+ * Rounding", paragraph "Cost".  This two-pass schedule keeps the FP32
+ * accumulators A = tK and B = rK in registers, so only the row statistics and
+ * z reach memory; gpa_attn_bwd_atomic_workspace_bytes sizes Algorithm 1's
+ * schedule with its FP32 accumulators.)
  */
 size_t gpa_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d, int mode);
 
