@@ -105,7 +105,8 @@ __device__ __forceinline__ void dq_probs(const f32x4 (&s)[2], const f32x4 (&dp)[
 }
 
 template <int D, bool GPROJ, bool WRITE_Z, int NB = 2>
-__global__ __launch_bounds__(kThreads * 2 / NB, D == 64 ? GPA_DQ_OCC64 : 2 / NB) void bwd_dq_kernel(
+__global__ __launch_bounds__(kThreads * 2 / NB, D == 64 ? GPA_DQ_OCC64 : 2 / NB)
+void bwd_dq_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, const uint16_t* __restrict__ O,
     const uint16_t* __restrict__ dO, const float* __restrict__ LSE, float* __restrict__ D_out,
@@ -143,7 +144,7 @@ __global__ __launch_bounds__(kThreads * 2 / NB, D == 64 ? GPA_DQ_OCC64 : 2 / NB)
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, c16 = lane & 15;
-    const int qh = wave % QG;  // which 16 NB of the workgroup's 64 queries
+    const int qh = wave % QG;  // which 16 NB-row group of the workgroup's 64 queries
     const int kh = wave / QG;  // which 32 of each 64-key tile
     const int q0w = tile * kTile + 16 * NB * qh;
 
